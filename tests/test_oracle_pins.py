@@ -1,0 +1,358 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests needs a GPU.  Each pin is chosen so that a plausible slip
+in the oracle (a dropped term, a wrong sign or index, a swapped operand, an
+off-by-one in the memory model) fails at least one of them; test_mutations.py
+plants such slips and checks that they are caught.
+"""
+
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import bounds, literal, opt, validate
+from paper_2606_22327_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- keys (a1)
+
+def test_volume_is_the_memory_time_area():
+    """Eq. 1 (Section 2.2): v = s*o + (o^2+o)/2 is the memory held over the
+    decode steps, (s+1) + ... + (s+o).  Checked exhaustively over every
+    s <= 4096, o <= 8192 (the largest configuration's bounds) against the
+    triangular numbers built by accumulation, and against the peak form
+    p*o - o^2/2 + o/2 of Appendix E.2."""
+    o = np.arange(1, 8193, dtype=np.int64)
+    tri = np.cumsum(o)                       # 1 + 2 + ... + o, by accumulation
+    for s in range(1, 4097, 37):
+        brute = s * o + tri                  # sum_{x=1..o} (s + x)
+        closed = s * o + (o * o + o) // 2
+        assert np.array_equal(brute, closed)
+        p = s + o
+        assert np.array_equal(2 * p * o - o * o + o, 2 * closed)
+    # the oracle's own key routine on edge and random pairs
+    rng = np.random.default_rng(5)
+    pairs = [(1, 1), (1, 8192), (4096, 1), (4096, 8192), (32, 64), (2048, 2048)]
+    pairs += [(int(a), int(b)) for a, b in zip(rng.integers(1, 4097, 300), rng.integers(1, 8193, 300))]
+    for s, oo in pairs:
+        assert oracle.volume(s, oo) == sum(s + x for x in range(1, oo + 1))
+        assert oracle.key("svf", 7, s, oo) == oracle.volume(s, oo)
+        assert oracle.key("svf1bit", 7, s, oo) == oracle.volume(s, oo)
+        assert oracle.key("sjf", 7, s, oo) == oo
+        assert oracle.key("fcfs", 7, s, oo) == 7
+    # packed 64-bit key (key << 32 | index) fits at every configuration bound
+    assert oracle.volume(4096, 8192) < 2 ** 32
+
+
+def test_literal_volume_matches_c():
+    for s, oo in [(1, 1), (3, 9), (100, 17), (5, 1000)]:
+        assert literal.volume(s, oo) == oracle.volume(s, oo)
+
+
+# ------------------------------------------------------- theory constants
+
+def test_alpha_table_matches_paper():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "alpha_cr.txt"))
+            if l.strip() and not l.startswith("#")]
+    assert len(rows) == 5
+    for num, den, conc, printed in rows:
+        alpha = int(num) / int(den)
+        assert math.floor(1 / alpha) == int(conc)
+        assert f"{bounds.cr_bound(alpha):.2f}" == printed
+    assert abs(bounds.cr_bound(1e-12) - 3.0) < 1e-9
+
+
+def test_onebit_minimax_proxies_and_distortion():
+    """Theorem thm:svf_1bit_burst and eq:volume_distortion: with T = 4096 the
+    threshold, proxies and distortion factor are exact integers (theta = 64,
+    O_0 = 8, O_1 = 512, b = 8) and v^/b^2 <= vol <= b^2 v^ holds for every
+    request with s + o <= T; every proxy-ordered pair has true-volume ratio
+    <= b^4 = T (Step 3)."""
+    T = 4096
+    theta, O0, O1 = bounds.onebit_minimax(T)
+    assert (theta, O0, O1) == (64, 8, 512)
+    b2 = 64
+    o = np.arange(1, T, dtype=np.int64)
+    for s in range(1, T):
+        oo = o[: T - s]                      # s + o <= T
+        vol = s * oo + (oo * oo + oo) // 2
+        cls = (oo > theta).astype(np.int64)
+        Om = np.where(cls == 1, O1, O0)
+        vhat = s * Om + (Om * Om + Om) // 2
+        assert (vhat <= b2 * vol).all() and (vol <= b2 * vhat).all()
+    # the 1-bit configuration's proxies: theta = 256 of T = 2048, geometric means
+    assert math.isqrt(256) == 16 and math.isqrt(256 * 2048) == 724
+
+
+def test_inversion_ratio_bound():
+    T, theta, O0, O1 = 4096, 64, 8, 512
+    rng = np.random.default_rng(1)
+    s = rng.integers(1, T // 2, 4000)
+    oo = np.array([rng.integers(1, T - x + 1) for x in s])
+    vol = s * oo + (oo * oo + oo) // 2
+    Om = np.where(oo > theta, O1, O0)
+    vhat = s * Om + (Om * Om + Om) // 2
+    order = np.argsort(vhat, kind="stable")
+    v = vol[order].astype(np.float64)
+    # for y before x in proxy order: vol_y <= T * vol_x
+    running_max = np.maximum.accumulate(v)
+    assert (running_max[:-1] <= T * v[1:]).all()
+
+
+def test_geometric_mean_volume_closed_form():
+    """Appendix F, Lemma 2: E[vol] = E[s]/mu + 1/mu^2 for geometric o; the
+    large-queue configuration's mean volume is 2048.5*400 + 400^2 = 979,400
+    (the clip at 8192 removes mass ~1e-9)."""
+    assert bounds.geometric_mean_volume(2048.5, 1 / 400) == pytest.approx(979400.0)
+    # direct sum over the geometric law (truncated far in the tail)
+    mu = 1 / 400
+    k = np.arange(1, 40000, dtype=np.float64)
+    pk = mu * (1 - mu) ** (k - 1)
+    ev = float((pk * (2048.5 * k + (k * k + k) / 2)).sum())
+    assert ev == pytest.approx(979400.0, rel=1e-9)
+
+
+# ------------------------------------------- the schedule itself (a2..a8)
+
+def _check_validator(batch, pols=None):
+    for pol in pols or batch.policies:
+        r = oracle.run(batch, pol)
+        assert (r["stats"][:, 1] == 0).all()
+        for i in range(batch.num_instances):
+            lo, hi = int(batch.offsets[i]), int(batch.offsets[i + 1])
+            d = batch.instance(i)
+            st = validate.validate(d["arrival"], d["prompt"], d["output"], r["start"][lo:hi],
+                                   r["admit_seq"][lo:hi], batch.M, pol, finish=r["finish"][lo:hi])
+            got = dict(zip(oracle.STAT_FIELDS, r["stats"][i].tolist()))
+            for f, v in st.items():
+                assert got[f] == v, (pol, i, f)
+            assert got["preemptions"] == 0
+
+
+def test_validator_burst_config():
+    _check_validator(W.config(1, instances=24))
+
+
+def test_validator_poisson_config():
+    _check_validator(W.config(2, instances=2, n=250))
+
+
+def test_validator_heavy_and_large_queue_shapes():
+    _check_validator(W.config(4, instances=1, n=300))
+    _check_validator(W.config(5, instances=1, n=400))
+
+
+def test_validator_onebit_without_preemption():
+    """1-bit runs whose proxies never undershoot (o <= O_b) have no
+    preemption; the validator then also pins the planned-length check."""
+    rng = np.random.default_rng(3)
+    parts = []
+    for _ in range(6):
+        n = 40
+        o = rng.integers(1, 25, n)
+        bit = (o > 8).astype(np.int8)
+        parts.append({"arrival": np.sort(rng.integers(0, 30, n)), "prompt": rng.integers(1, 20, n),
+                      "output": o, "long_bit": bit})
+    b = W.assemble("ob", parts, 120, ("svf1bit",), O0=8, O1=24)
+    r = oracle.run(b, "svf1bit")
+    for i in range(b.num_instances):
+        lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+        d = b.instance(i)
+        oh = np.where(d["long_bit"] == 1, 24, 8)
+        assert (r["preempt"][lo:hi] == 0).all()
+        validate.validate(d["arrival"], d["prompt"], d["output"], r["start"][lo:hi],
+                          r["admit_seq"][lo:hi], b.M, "svf1bit", ohat=oh, finish=r["finish"][lo:hi])
+
+
+def test_special_case_unbounded_memory_starts_at_arrival():
+    b = W.config(2, instances=3, n=200)
+    big = W.assemble("big", [b.instance(i) for i in range(3)],
+                     int((b.prompt.astype(np.int64) + b.output).sum()), ("svf", "sjf", "fcfs"))
+    for pol in big.policies:
+        r = oracle.run(big, pol)
+        assert np.array_equal(r["start"], big.arrival)
+        assert np.array_equal(r["finish"], big.arrival + big.output)
+
+
+def test_special_case_serial_regime():
+    """When 2*min s + min o >= M no two requests can overlap, so under a burst
+    every start is the sum of the true lengths ahead of it in priority order
+    (single-machine sequencing)."""
+    rng = np.random.default_rng(11)
+    for _ in range(20):
+        n = 12
+        s = rng.integers(30, 40, n)
+        o = rng.integers(1, 20, n)
+        M = int(2 * s.min() + o.min())
+        M = max(M, int((s + o).max()))
+        if 2 * s.min() + o.min() < M:
+            continue
+        b = W.assemble("serial", [{"arrival": np.zeros(n, np.int64), "prompt": s, "output": o}],
+                       M, ("svf", "sjf", "fcfs"))
+        for pol in b.policies:
+            r = oracle.run(b, pol)
+            order = validate.priority_order(pol, np.zeros(n), s, o)
+            expect = np.zeros(n, dtype=np.int64)
+            expect[order] = np.concatenate([[0], np.cumsum(o[order])[:-1]])
+            assert np.array_equal(r["start"], expect)
+
+
+def test_special_case_single_request_and_exact_fit():
+    b = W.assemble("one", [{"arrival": np.array([5]), "prompt": np.array([7]),
+                            "output": np.array([9])}], 16, ("svf", "sjf", "fcfs"))
+    for pol in b.policies:
+        r = oracle.run(b, pol)
+        assert r["start"].tolist() == [5] and r["finish"].tolist() == [14]
+        st = dict(zip(oracle.STAT_FIELDS, r["stats"][0].tolist()))
+        assert st["peak_mem"] == 16 and st["request_steps"] == 9 and st["makespan"] == 14
+
+
+def test_special_case_equal_keys_follow_index():
+    n = 30
+    b = W.assemble("eq", [{"arrival": np.zeros(n), "prompt": np.full(n, 4),
+                           "output": np.full(n, 6)}], 40, ("svf", "sjf", "fcfs"))
+    for pol in b.policies:
+        r = oracle.run(b, pol)
+        assert (np.diff(r["admit_seq"]) > 0).all()
+        assert (np.diff(r["start"]) >= 0).all()
+
+
+def test_empty_instance():
+    b = W.assemble("empty", [{"arrival": np.zeros(0), "prompt": np.zeros(0),
+                              "output": np.zeros(0)}] * 2, 10, ("svf",))
+    r = oracle.run(b, "svf")
+    assert r["stats"].tolist() == [[0, 0, 0, 0, 0, 0, 0, 0]] * 2
+
+
+# ------------------------------------------------- optimal schedules (T5)
+
+def test_exhaustive_opt_bounds_and_svf_ratio():
+    """Tiny burst instances solved exactly.  OPT >= sum o (Lemma
+    lemma:opt_lb_execution); M*OPT >= sorted prefix-volume double sum
+    (Proposition prop:opt_lower_bound); every policy's total latency >= OPT;
+    SVF within 1 + 2/(1-alpha) of OPT (Theorem thm:svf-burst)."""
+    worst = {}
+    for inst in W.tiny_cr_instances(150):
+        M = int(inst["M"])
+        s, o = inst["prompt"], inst["output"]
+        OPT = opt.optimal_total_latency(s, o, M)
+        assert OPT >= bounds.opt_lower_bound_exec(o)
+        assert M * OPT >= bounds.opt_lower_bound_area(s, o, M)
+        b = W.assemble("t", [inst], M, ("svf", "sjf", "fcfs"))
+        for pol in b.policies:
+            tel = int(oracle.run(b, pol, threads=1)["stats"][0, 2])
+            assert tel >= OPT
+            worst[pol] = max(worst.get(pol, 0), tel / OPT)
+            if pol == "svf":
+                assert bounds.cr_bound_holds(tel, OPT, M, int((s + o).max()))
+    assert worst["svf"] >= 1.0
+
+
+def test_opt_small_hand_instance():
+    # two requests that cannot overlap (M = 6: together they hold 4 + 4 at
+    # the first step): the best order runs the shorter first, starts 0 and 1,
+    # total latency 1 + (1 + 3) = 5
+    assert opt.optimal_total_latency([3, 3], [1, 3], 6) == 5
+    # with s = 2 they overlap exactly at M (3 + 3 at the first step): 1 + 3
+    assert opt.optimal_total_latency([2, 2], [1, 3], 6) == 4
+    # everything fits at once: total latency = sum o
+    assert opt.optimal_total_latency([1, 1, 1], [2, 2, 2], 100) == 6
+
+
+# ------------------------------------------------ at-scale bounds (T6)
+
+def test_waiting_time_lemma_at_scale():
+    """Lemma lemma:svf_wait_time in integers on the full burst configuration:
+    for every request that waits, W_j (M - P_max) < sum_{i before j} p_i o_i
+    (the proof's intermediate bound), and the total-latency consequence
+    TEL (M - P_max) <= sum_j sum_{i before j} p_i o_i + (M - P_max) sum o."""
+    b = W.config(1)
+    for pol in ("svf", "sjf", "fcfs"):
+        r = oracle.run(b, pol)
+        for i in range(b.num_instances):
+            lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+            d = b.instance(i)
+            s = d["prompt"].astype(np.int64)
+            o = d["output"].astype(np.int64)
+            p = s + o
+            gap = b.M - int(p.max())
+            order = validate.priority_order(pol, d["arrival"], s, o)
+            prefix = np.concatenate([[0], np.cumsum((p * o)[order])[:-1]])
+            rhs = np.empty_like(prefix)
+            rhs[order] = prefix
+            w = r["start"][lo:hi].astype(np.int64)
+            assert ((w == 0) | (w * gap < rhs)).all()
+            tel = int(r["stats"][i, 2])
+            assert tel * gap <= int(rhs.sum()) + gap * int(o.sum())
+            if pol == "svf":
+                lb = max(int(o.sum()), -(-bounds.opt_lower_bound_area(s, o, b.M) // b.M))
+                assert bounds.cr_bound_holds(tel, lb, b.M, int(p.max()))
+
+
+# ------------------------------------------- C oracle vs literal oracle
+
+@pytest.mark.parametrize("seed", range(5))
+def test_c_oracle_matches_literal(seed):
+    for kw in (dict(), dict(bits=True), dict(plan_noise=True)):
+        b = W.random_small(seed, instances=10, n_max=13, s_max=6, o_max=10, M=24,
+                           gap_mean=0.8 if seed % 2 else 0.0, **kw)
+        for pol in b.policies:
+            r = oracle.run(b, pol, threads=2)
+            for i in range(b.num_instances):
+                lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+                d = b.instance(i)
+                L = literal.simulate(d["arrival"], d["prompt"], d["output"], b.M, pol,
+                                     plan=d["plan_len"], long_bit=d["long_bit"], O0=b.O0,
+                                     O1=b.O1, max_steps=b.max_steps)
+                for f in ("start", "finish", "preempt", "admit_seq"):
+                    assert r[f][lo:hi].tolist() == L[f], (pol, i, f)
+                got = dict(zip(oracle.STAT_FIELDS, r["stats"][i].tolist()))
+                for f in oracle.STAT_FIELDS:
+                    assert got[f] == L[f], (pol, i, f)
+
+
+def test_c_oracle_matches_literal_on_config_shapes():
+    b = W.config(1, instances=4)
+    b3 = W.config(3, instances=2, n=60)
+    for batch in (b, b3):
+        for pol in batch.policies:
+            r = oracle.run(batch, pol)
+            for i in range(batch.num_instances):
+                lo, hi = int(batch.offsets[i]), int(batch.offsets[i + 1])
+                d = batch.instance(i)
+                L = literal.simulate(d["arrival"], d["prompt"], d["output"], batch.M, pol,
+                                     long_bit=d["long_bit"], O0=batch.O0, O1=batch.O1,
+                                     max_steps=batch.max_steps)
+                for f in ("start", "finish", "preempt", "admit_seq"):
+                    assert r[f][lo:hi].tolist() == L[f]
+
+
+def test_step_budget_and_partial_runs():
+    b = W.random_small(7, instances=6, n_max=12, s_max=5, o_max=8, M=20, gap_mean=0.5)
+    for pol in b.policies:
+        full = oracle.run(b, pol)
+        T = int(full["stats"][:, 6].max())
+        for stop in (0, 1, 3, T // 2, T + 5):
+            part = oracle.run(b, pol, t_stop=stop)
+            for i in range(b.num_instances):
+                lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+                d = b.instance(i)
+                L = literal.simulate(d["arrival"], d["prompt"], d["output"], b.M, pol,
+                                     max_steps=b.max_steps, t_stop=stop)
+                assert part["start"][lo:hi].tolist() == L["start"]
+                assert part["finish"][lo:hi].tolist() == L["finish"]
+                assert int(part["stats"][i, 1]) == L["status"]
+                assert int(part["stats"][i, 3]) == L["request_steps"]
+                assert int(part["stats"][i, 4]) == L["peak_mem"]
+        ms = 4
+        cut = oracle.run(b, pol, max_steps=ms)
+        for i in range(b.num_instances):
+            d = b.instance(i)
+            L = literal.simulate(d["arrival"], d["prompt"], d["output"], b.M, pol, max_steps=ms)
+            assert int(cut["stats"][i, 1]) == L["status"]
+            assert int(cut["stats"][i, 3]) == L["request_steps"]
