@@ -56,18 +56,21 @@ def true_profile(s, o, start, horizon):
     """mem[tau] for tau in [0, horizon]; a request started at k adds s+tau-k
     for tau in [k+1, k+o].  Built with two difference arrays (slope and
     intercept), independently of any simulator."""
+    s = np.asarray(s, dtype=np.int64)
+    o = np.asarray(o, dtype=np.int64)
+    k = np.asarray(start, dtype=np.int64)
+    keep = k >= 0
+    s, o, k = s[keep], o[keep], k[keep]
+    lo = k + 1
+    hi = np.minimum(k + o, horizon)
+    keep = lo <= hi
+    s, k, lo, hi = s[keep], k[keep], lo[keep], hi[keep]
     slope = np.zeros(horizon + 2, dtype=np.int64)
     icpt = np.zeros(horizon + 2, dtype=np.int64)
-    for sv, ov, k in zip(s.tolist(), o.tolist(), start.tolist()):
-        if k < 0:
-            continue
-        lo, hi = k + 1, min(k + ov, horizon)
-        if lo > hi:
-            continue
-        slope[lo] += 1
-        slope[hi + 1] -= 1
-        icpt[lo] += sv - k
-        icpt[hi + 1] -= sv - k
+    np.add.at(slope, lo, 1)
+    np.add.at(slope, hi + 1, -1)
+    np.add.at(icpt, lo, s - k)
+    np.add.at(icpt, hi + 1, -(s - k))
     tau = np.arange(horizon + 2, dtype=np.int64)
     return (np.cumsum(slope) * tau + np.cumsum(icpt))[: horizon + 1]
 

@@ -1,0 +1,46 @@
+"""Build the HIP library ``libsvfsim.so`` for gfx950 with hipcc.
+
+The library holds every kernel of the simulator and the host runtime behind
+the C ABI of ``include/svfsim.h``.  It is built in-tree so that the same file
+is loaded by the tests, the smoke check and the benchmark.
+"""
+
+import os
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(ROOT, "_build")
+LIB = os.path.join(PKG, "libsvfsim.so")
+
+ARCH = os.environ.get("SVFSIM_ARCH", "gfx950")
+# Packed FP32 instructions are kept out of every code object.
+GPU_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
+
+
+def _run(cmd):
+    subprocess.check_call(cmd)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    kern_o = os.path.join(BUILD, "svf_kernels.o")
+    rt_o = os.path.join(BUILD, "svf_runtime.o")
+    _run(["hipcc", f"--offload-arch={ARCH}", *COMMON, *GPU_FLAGS, "-c",
+          os.path.join(CSRC, "svf_kernels.hip"), "-o", kern_o])
+    _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "svf_runtime.cpp"), "-o", rt_o])
+    tmp = LIB + ".tmp"
+    _run(["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_o, rt_o, "-o", tmp])
+    os.replace(tmp, LIB)
+    if verbose:
+        print(LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    build(verbose=True)
+    sys.exit(0)

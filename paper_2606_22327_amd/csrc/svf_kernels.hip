@@ -1,0 +1,742 @@
+// svf_kernels.hip -- gfx950 kernels of the batched scheduling simulator.
+//
+// One "segment" is one instance under one policy; segments are independent.
+// Kernels, in launch order:
+//   k_fill_*          clear state, bitmaps, rings and outputs (no memset nodes)
+//   k_chunk_sort<CH>  priority keys (Eq. 1 / Eq. 2) packed as key<<32|index and
+//                     bitonic-sorted in LDS, one workgroup per chunk of CH
+//   k_merge_pass      doubles the sorted run length of segments longer than CH
+//                     (each element finds its output slot by binary search in
+//                     the partner run)
+//   k_build_rec       rank-ordered request records and the index->rank map
+//   k_sim<D_LDS>      the simulation: one wave64 per segment
+//   k_finalize        per-request outputs as of the reached step + per-segment
+//                     statistics
+//
+// Waiting set.  A segment's requests are sorted once by priority; the waiting
+// set is then a bitmap over priority ranks (bit r set iff the request of rank
+// r has arrived and is not running), with a summary word per 64 bitmap words.
+// The highest-priority waiting request is the lowest set bit: one ballot over
+// at most 64 summary words, then two count-trailing-zeros.  Both levels live
+// in LDS for the whole launch.
+//
+// Future memory profile.  D[tau mod H] holds the memory that the running
+// requests are planned to hold at future step tau (each request started at k
+// with planned length L adds s + (tau - k) for tau in [k+1, k+L]; Section 3.1,
+// eq:c2).  H is a power of two >= the longest planned length, so the window
+// [t+1, t+H] never wraps onto itself.  The forward-looking check of a
+// candidate h at step t (no future step above M; Appendix E.2) is then one
+// pass over its own window: max_{j<o^_h} D[t+1+j] + (s_h + j + 1) <= M.
+// Admitting h adds its growth to the same window; a step that becomes past is
+// folded into the peak statistic and cleared.
+//
+// Known lengths (the scheduler plans with the true length) make D change only
+// at admissions, so a blocked head stays blocked until a computable step t_f
+// (every violating tau stops violating once t >= min(tau, D[tau]+tau+s_h-M))
+// or until a request of higher priority arrives.  Such segments jump from
+// event to event; the skipped steps are exactly the ones where the per-step
+// scheduler admits nothing.  Segments whose planned lengths differ from the
+// truth (1-bit SVF, noisy predictions) are advanced one step at a time: they
+// track true completions, requests running past their planned length (planned
+// to finish at the next step, kept as two running sums), and evictions when the
+// true memory of the next step would exceed M.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "svf_kernels.h"
+
+namespace svfk {
+
+// ------------------------------------------------------------ wave helpers
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __ballot(p); }
+
+__device__ __forceinline__ int wave_max_i32(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ __forceinline__ int wave_min_i32(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+    return v;
+}
+
+__device__ __forceinline__ long long wave_sum_i64(long long v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+__device__ __forceinline__ long long wave_max_i64(long long v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        long long w = __shfl_xor(v, o);
+        v = w > v ? w : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ int bcast_i32(int v, int src) { return __shfl(v, src); }
+
+__device__ __forceinline__ void wave_sync() { __syncthreads(); }
+
+// The planned length the scheduler uses for request i under a policy.
+__device__ __forceinline__ int planned_len(int policy, const int32_t* o, const int32_t* plan,
+                                           const int8_t* bit, int O0, int O1, int64_t i) {
+    if (policy == POLICY_SVF1BIT) return bit[i] ? O1 : O0;
+    return plan ? plan[i] : o[i];
+}
+
+// Priority key (lower runs first): Section 2.2, Eq. 1 (volume) and Eq. 2 (the
+// same volume with the 1-bit proxy length), SJF by length, FCFS by arrival.
+__device__ __forceinline__ uint64_t priority_key(int policy, int32_t a, int32_t s, int32_t oh) {
+    if (policy == POLICY_FCFS) return (uint64_t)(uint32_t)a;
+    if (policy == POLICY_SJF) return (uint64_t)(uint32_t)oh;
+    const uint64_t L = (uint64_t)(uint32_t)oh;
+    return (uint64_t)(uint32_t)s * L + ((L * L + L) >> 1);
+}
+
+// ------------------------------------------------------------ fills
+
+__global__ void k_fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+__global__ void k_fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+__global__ void k_init_state(SegState* __restrict__ st, int32_t G) {
+    int g = blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= G) return;
+    SegState z;
+    z.t = 0; z.cursor = 0; z.seq = 0; z.status = STATUS_RUNNING;
+    z.nA = 0; z.nfin = 0; z.max_fin = 0; z.head_rank = -1;
+    z.t_f = 0; z.N_O = 0; z.C_O = 0; z.peak = 0; z.req_steps = 0; z.pad = 0;
+    st[g] = z;
+}
+
+// ------------------------------------------------------------ keys and sort
+
+template <int CH, int NT>
+__global__ __launch_bounds__(NT) void k_chunk_sort(SortArgs A) {
+    __shared__ uint64_t sk[CH];
+    const int c = blockIdx.x;
+    const int g = A.chunk_seg[c];
+    const int lo = A.chunk_lo[c];
+    const int pol = g / A.I, inst = g - pol * A.I;
+    const int64_t off = A.offsets[inst];
+    const int n = (int)(A.offsets[inst + 1] - off);
+    const int len = min(CH, n - lo);
+    const int policy = A.policies[pol];
+    for (int j = threadIdx.x; j < CH; j += NT) {
+        uint64_t v = ~0ull;
+        if (j < len) {
+            const int64_t i = off + lo + j;
+            const int oh = planned_len(policy, A.o, A.plan, A.bit, A.O0, A.O1, i);
+            v = (priority_key(policy, A.a[i], A.s[i], oh) << 32) | (uint32_t)(lo + j);
+        }
+        sk[j] = v;
+    }
+    __syncthreads();
+    for (int k = 2; k <= CH; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int t = threadIdx.x; t < CH / 2; t += NT) {
+                const int i = 2 * t - (t & (j - 1));
+                const int l = i + j;
+                const bool asc = (i & k) == 0;
+                const uint64_t x = sk[i], y = sk[l];
+                if ((x > y) == asc) { sk[i] = y; sk[l] = x; }
+            }
+            __syncthreads();
+        }
+    }
+    uint64_t* out = A.keys_out + (int64_t)pol * A.N + off + lo;
+    for (int j = threadIdx.x; j < len; j += NT) out[j] = sk[j];
+}
+
+// One merge level: runs of length w become runs of length 2w.  Keys are
+// unique (the index is packed in), so "number of partner elements below x"
+// is the exact displacement.
+__global__ __launch_bounds__(256) void k_merge_pass(SortArgs A, int w) {
+    const int c = blockIdx.x;
+    const int g = A.chunk_seg[c];
+    const int lo = A.chunk_lo[c];
+    const int pol = g / A.I, inst = g - pol * A.I;
+    const int64_t off = A.offsets[inst];
+    const int n = (int)(A.offsets[inst + 1] - off);
+    const int len = min(A.CH, n - lo);
+    const uint64_t* in = A.keys_in + (int64_t)pol * A.N + off;
+    uint64_t* out = A.keys_out + (int64_t)pol * A.N + off;
+    for (int j = threadIdx.x; j < len; j += blockDim.x) {
+        const int p = lo + j;
+        const uint64_t x = in[p];
+        const int q = p / w;
+        const int pair_base = (q >> 1) * 2 * w;
+        const int local = p - q * w;
+        int plo, phi;  // partner run [plo, phi)
+        if ((q & 1) == 0) { plo = (q + 1) * w; phi = min(n, plo + w); }
+        else { plo = (q - 1) * w; phi = plo + w; }
+        int below = 0;
+        if (plo < phi) {
+            int L = plo, R = phi;  // first element >= x
+            while (L < R) {
+                const int m = (L + R) >> 1;
+                if (in[m] < x) L = m + 1; else R = m;
+            }
+            below = L - plo;
+        }
+        out[pair_base + local + below] = x;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_build_rec(SortArgs A) {
+    const int c = blockIdx.x;
+    const int g = A.chunk_seg[c];
+    const int lo = A.chunk_lo[c];
+    const int pol = g / A.I, inst = g - pol * A.I;
+    const int64_t off = A.offsets[inst];
+    const int n = (int)(A.offsets[inst + 1] - off);
+    const int len = min(A.CH, n - lo);
+    const int policy = A.policies[pol];
+    const uint64_t* keys = A.keys_in + (int64_t)pol * A.N + off;
+    int4* rec = A.rec + (int64_t)pol * A.N + off;
+    int32_t* rank = A.rank + (int64_t)pol * A.N + off;
+    for (int j = threadIdx.x; j < len; j += blockDim.x) {
+        const int r = lo + j;
+        const int idx = (int)(uint32_t)keys[r];
+        if ((unsigned)idx >= (unsigned)n) continue;  // only a broken sort gets here
+        const int64_t i = off + idx;
+        int4 q;
+        q.x = idx;
+        q.y = A.s[i];
+        q.z = planned_len(policy, A.o, A.plan, A.bit, A.O0, A.O1, i);
+        q.w = A.o[i];
+        rec[r] = q;
+        rank[idx] = r;
+    }
+}
+
+// ------------------------------------------------------------ simulation
+
+struct Seg {
+    int n;
+    const int4* __restrict__ rec;
+    const int32_t* __restrict__ rank;
+    const int32_t* __restrict__ a;
+    int32_t* __restrict__ start;
+    int32_t* __restrict__ fin;
+    int32_t* __restrict__ preempt;
+    int32_t* __restrict__ admit_seq;
+    int32_t* __restrict__ act;
+    int32_t* __restrict__ evl;
+};
+
+// Lowest set bit of the two-level rank bitmap, or -1.
+__device__ __forceinline__ int bitmap_first(const uint64_t* B, const uint64_t* S, int W1) {
+    const int lane = lane_id();
+    for (int base = 0; base < W1; base += 64) {
+        const uint64_t v = (base + lane < W1) ? S[base + lane] : 0ull;
+        const uint64_t m = ballot(v != 0ull);
+        if (m) {
+            const int f = __builtin_ctzll(m);
+            const uint64_t sv = __shfl(v, f);
+            const int w = (base + f) * 64 + __builtin_ctzll(sv);
+            const uint64_t bw = B[w];
+            return w * 64 + __builtin_ctzll(bw);
+        }
+    }
+    return -1;
+}
+
+__device__ __forceinline__ void bitmap_set_atomic(uint64_t* B, uint64_t* S, int r) {
+    const int w = r >> 6;
+    atomicOr((unsigned long long*)&B[w], 1ull << (r & 63));
+    atomicOr((unsigned long long*)&S[w >> 6], 1ull << (w & 63));
+}
+
+// called by one lane
+__device__ __forceinline__ void bitmap_clear(uint64_t* B, uint64_t* S, int r) {
+    const int w = r >> 6;
+    const uint64_t nb = B[w] & ~(1ull << (r & 63));
+    B[w] = nb;
+    if (nb == 0ull) S[w >> 6] &= ~(1ull << (w & 63));
+}
+
+// Arrivals at step t: the requests [cursor, ...) with a == t form a prefix
+// (arrivals are sorted).  Sets their rank bits; returns the smallest new rank.
+__device__ __forceinline__ int ingest_arrivals(const Seg& sg, uint64_t* B, uint64_t* S, int t,
+                                               int& cursor) {
+    const int lane = lane_id();
+    int min_rank = INT32_MAX;
+    while (cursor < sg.n) {
+        const int i = cursor + lane;
+        const bool arr = (i < sg.n) && (sg.a[i] == t);
+        const uint64_t m = ballot(arr);
+        if (m == 0ull) break;
+        int r = INT32_MAX;
+        if (arr) {
+            r = sg.rank[i];
+            if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
+            else r = INT32_MAX;
+        }
+        min_rank = min(min_rank, wave_min_i32(r));
+        const int cnt = __popcll(m);
+        cursor += cnt;
+        if (cnt < 64) break;
+    }
+    wave_sync();
+    return min_rank;
+}
+
+// Forward-looking check of a candidate (size s_h, planned length oh) at step t.
+// extra1 is added at tau = t+1 (requests running past their plan).  Returns
+// true if it fits; otherwise *t_free receives the first step at which every
+// violation seen in this window has disappeared (valid while D is unchanged).
+template <typename DPtr>
+__device__ __forceinline__ bool check_fit(DPtr D, int Hm, int t, int s_h, int oh, int M,
+                                          int64_t extra1, int* t_free) {
+    const int lane = lane_id();
+    const int X = M - s_h;
+    bool viol = false;
+    int rel = INT32_MIN;
+    for (int j = lane; j < oh; j += 64) {
+        const int tau = t + 1 + j;
+        int64_t v = (int64_t)D[tau & Hm] + (j + 1);
+        if (j == 0) v += extra1;
+        if (v > X) {
+            viol = true;
+            const int64_t r = (int64_t)t + (v - X);
+            rel = max(rel, (int)min((int64_t)tau, r));
+        }
+    }
+    const bool fits = ballot(viol) == 0ull;
+    if (!fits) *t_free = wave_max_i32(rel);
+    return fits;
+}
+
+template <typename DPtr>
+__device__ __forceinline__ void add_growth(DPtr D, int Hm, int t, int s_h, int oh) {
+    for (int j = lane_id(); j < oh; j += 64) D[(t + 1 + j) & Hm] += s_h + j + 1;
+}
+
+// remove the planned profile of a request started at k with planned length L
+// for the future steps tau in [t+1, k+L]
+template <typename DPtr>
+__device__ __forceinline__ void remove_future(DPtr D, int Hm, int t, int s, int k, int L) {
+    const int cnt = k + L - t;
+    for (int j = lane_id(); j < cnt; j += 64) {
+        const int tau = t + 1 + j;
+        D[tau & Hm] -= s + (tau - k);
+    }
+}
+
+// fold the final steps [t+1, t+len] into the peak and clear them
+template <typename DPtr>
+__device__ __forceinline__ int fold_past(DPtr D, int Hm, int t, int len) {
+    int pm = 0;
+    for (int j = lane_id(); j < len; j += 64) {
+        const int slot = (t + 1 + j) & Hm;
+        pm = max(pm, (int)D[slot]);
+        D[slot] = 0;
+    }
+    return wave_max_i32(pm);
+}
+
+// ---- known lengths: event-driven
+
+template <typename DPtr>
+__device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
+                          DPtr D, SegState& st, int t_lim) {
+    const int lane = lane_id();
+    const int Hm = P.H - 1;
+    const int M = P.M;
+    int t = st.t, cursor = st.cursor, seq = st.seq, nadm = st.nfin, max_fin = st.max_fin;
+    int head = st.head_rank, t_f = st.t_f;
+    int64_t peak = st.peak;
+    int status = STATUS_RUNNING;
+    for (;;) {
+        // every request finished by step t-1 (an empty instance is done at t = 0)
+        if (nadm == sg.n && (nadm == 0 || max_fin <= t - 1)) { status = STATUS_DONE; break; }
+        if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
+        if (t >= t_lim) break;
+        // 1. arrivals
+        const int new_min = ingest_arrivals(sg, B, S, t, cursor);
+        // 4. admissions (known lengths: completions change nothing ahead)
+        if (head < 0 || new_min < head || t >= t_f) {
+            for (;;) {
+                const int r = bitmap_first(B, S, W1);
+                if (r < 0) { head = -1; break; }
+                const int4 q = sg.rec[r];
+                int tf = 0;
+                if (!check_fit(D, Hm, t, q.y, q.z, M, 0, &tf)) { head = r; t_f = tf; break; }
+                add_growth(D, Hm, t, q.y, q.z);
+                if (lane == 0) {
+                    bitmap_clear(B, S, r);
+                    sg.start[q.x] = t;
+                    sg.admit_seq[q.x] = seq;
+                    sg.fin[q.x] = t + q.w;
+                }
+                wave_sync();
+                ++seq;
+                ++nadm;
+                max_fin = max(max_fin, t + q.w);
+            }
+        }
+        // 5. advance to the next step where anything can happen
+        int nt;
+        const int next_arr = cursor < sg.n ? sg.a[cursor] : INT32_MAX;
+        if (head >= 0) nt = min(t_f, next_arr);
+        else if (cursor < sg.n) nt = next_arr;
+        else nt = max_fin + 1;
+        nt = max(nt, t + 1);
+        nt = min(nt, t_lim);
+        nt = min(nt, P.max_steps + 1);
+        if (nt <= t) nt = t + 1;
+        const int len = min(nt - t, P.H);
+        const int pm = fold_past(D, Hm, t, len);
+        wave_sync();
+        peak = max(peak, (int64_t)pm);
+        t = nt;
+    }
+    st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nadm; st.max_fin = max_fin;
+    st.head_rank = head; st.t_f = t_f; st.peak = peak; st.status = status;
+}
+
+// ---- planned lengths differ from the truth: one step at a time
+
+template <typename DPtr>
+__device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
+                            DPtr D, SegState& st, int t_lim) {
+    const int lane = lane_id();
+    const int Hm = P.H - 1;
+    const int M = P.M;
+    int t = st.t, cursor = st.cursor, seq = st.seq, nfin = st.nfin, nA = st.nA, N_O = st.N_O;
+    int64_t C_O = st.C_O, peak = st.peak, req_steps = st.req_steps;
+    int status = STATUS_RUNNING;
+    for (;;) {
+        if (nfin == sg.n) { status = STATUS_DONE; break; }
+        if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
+        if (t >= t_lim) break;
+        // 1. arrivals
+        ingest_arrivals(sg, B, S, t, cursor);
+        // 2. completions and requests reaching their planned length
+        {
+            int newA = 0;
+            int64_t dC = 0;
+            int dN = 0, dfin = 0;
+            for (int base = 0; base < nA; base += 64) {
+                const int x = base + lane;
+                int r = -1, idx = 0, s = 0, oh = 0, o = 0, k = 0;
+                bool live = x < nA, done = false;
+                if (live) {
+                    r = sg.act[x];
+                    const int4 q = sg.rec[r];
+                    idx = q.x; s = q.y; oh = q.z; o = q.w;
+                    k = sg.start[idx];
+                    const int e = t - k;
+                    if (e == o) {
+                        done = true;
+                        sg.fin[idx] = t;
+                        if (o > oh) { dC -= (int64_t)(s - k); dN -= 1; }
+                    } else if (e == oh) {
+                        dC += (int64_t)(s - k);
+                        dN += 1;
+                    }
+                }
+                // early finishers give back their planned future
+                uint64_t early = ballot(done && oh > o);
+                while (early) {
+                    const int src = __builtin_ctzll(early);
+                    early &= early - 1;
+                    const int ks = bcast_i32(k, src), ss = bcast_i32(s, src), ls = bcast_i32(oh, src);
+                    remove_future(D, Hm, t, ss, ks, ls);
+                }
+                const uint64_t keep = ballot(live && !done);
+                dfin += __popcll(ballot(done));
+                // in-place compaction: every kept entry moves to a lower or equal slot
+                const int pos = newA + __popcll(keep & ((1ull << lane) - 1ull));
+                wave_sync();
+                if (live && !done) sg.act[pos] = r;
+                newA += __popcll(keep);
+                wave_sync();
+            }
+            nA = newA;
+            C_O += wave_sum_i64(dC);
+            N_O += (int)wave_sum_i64(dN);
+            nfin += dfin;
+        }
+        // 3. overflow of the true memory at t+1: evict the largest believed
+        //    remaining volume (latest arrival on ties)
+        int nev = 0;
+        {
+            int64_t mem_next = (int64_t)D[(t + 1) & Hm] + C_O + (int64_t)N_O * (t + 1);
+            while (mem_next > M && nA > 0) {
+                long long bestR = -1;
+                int bestIdx = -1, bestPos = -1;
+                for (int x = lane; x < nA; x += 64) {
+                    const int4 q = sg.rec[sg.act[x]];
+                    const int k = sg.start[q.x];
+                    const long long e = t - k;
+                    const long long L = max((long long)q.z, e + 1);
+                    const long long R = (L - e) * q.y + (L * (L + 1) - e * (e + 1)) / 2;
+                    if (R > bestR || (R == bestR && q.x > bestIdx)) { bestR = R; bestIdx = q.x; bestPos = x; }
+                }
+                const long long gR = wave_max_i64(bestR);
+                const int gIdx = wave_max_i32(bestR == gR ? bestIdx : -1);
+                const uint64_t who = ballot(bestR == gR && bestIdx == gIdx);
+                const int src = __builtin_ctzll(who);
+                const int vpos = bcast_i32(bestPos, src);
+                const int vr = sg.act[vpos];
+                const int4 q = sg.rec[vr];
+                const int k = sg.start[q.x];
+                const int e = t - k;
+                if (e < q.z) remove_future(D, Hm, t, q.y, k, q.z);
+                else { C_O -= (int64_t)(q.y - k); N_O -= 1; }
+                mem_next -= (int64_t)q.y + (t + 1) - k;
+                wave_sync();
+                if (lane == 0) {
+                    sg.act[vpos] = sg.act[nA - 1];
+                    sg.preempt[q.x] += 1;
+                    sg.start[q.x] = -1;
+                    sg.admit_seq[q.x] = -1;
+                    sg.evl[nev] = vr;
+                }
+                wave_sync();
+                --nA;
+                ++nev;
+                // the ring entry at t+1 may have changed: recompute from parts
+                mem_next = (int64_t)D[(t + 1) & Hm] + C_O + (int64_t)N_O * (t + 1);
+            }
+        }
+        // 4. admissions
+        for (;;) {
+            const int r = bitmap_first(B, S, W1);
+            if (r < 0) break;
+            const int4 q = sg.rec[r];
+            int tf = 0;
+            const int64_t extra1 = C_O + (int64_t)N_O * (t + 1);
+            if (!check_fit(D, Hm, t, q.y, q.z, M, extra1, &tf)) break;
+            add_growth(D, Hm, t, q.y, q.z);
+            if (lane == 0) {
+                bitmap_clear(B, S, r);
+                sg.start[q.x] = t;
+                sg.admit_seq[q.x] = seq;
+                sg.act[nA] = r;
+            }
+            wave_sync();
+            ++seq;
+            ++nA;
+        }
+        // evicted requests compete again from the next step
+        for (int x = lane; x < nev; x += 64) {
+            const int r = sg.evl[x];
+            if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
+        }
+        wave_sync();
+        // 5. advance
+        req_steps += nA;
+        const int slot = (t + 1) & Hm;
+        const int64_t mem = (int64_t)D[slot] + C_O + (int64_t)N_O * (t + 1);
+        peak = max(peak, mem);
+        wave_sync();
+        if (lane == 0) D[slot] = 0;
+        wave_sync();
+        ++t;
+    }
+    st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nfin; st.nA = nA; st.N_O = N_O;
+    st.C_O = C_O; st.peak = peak; st.req_steps = req_steps; st.status = status;
+}
+
+template <bool D_LDS>
+__global__ __launch_bounds__(64) void k_sim(SimArgs P) {
+    extern __shared__ uint64_t smem[];
+    const int g = blockIdx.x;
+    const int lane = lane_id();
+    const int pol = g / P.I, inst = g - pol * P.I;
+    const int64_t off = P.offsets[inst];
+    const int n = (int)(P.offsets[inst + 1] - off);
+    SegState st = P.st[g];
+    if (st.status != STATUS_RUNNING) return;
+
+    Seg sg;
+    sg.n = n;
+    const int64_t base = (int64_t)pol * P.N + off;
+    sg.rec = P.rec + base;
+    sg.rank = P.rank + base;
+    sg.a = P.a + off;
+    sg.start = P.start + base;
+    sg.fin = P.fin + base;
+    sg.preempt = P.preempt + base;
+    sg.admit_seq = P.admit_seq + base;
+    sg.act = P.act ? P.act + base : nullptr;
+    sg.evl = P.evl ? P.evl + base : nullptr;
+
+    // rank bitmap (two levels) staged in LDS for the launch
+    const int W0 = (n + 63) >> 6;
+    const int W1 = (W0 + 63) >> 6;
+    const int64_t bw_base = (int64_t)pol * P.bw_total + P.bw_off[inst];
+    uint64_t* Bg = P.bitmap + bw_base;
+    uint64_t* B = smem;
+    uint64_t* S = smem + W0;
+    for (int x = lane; x < W0 + W1; x += 64) B[x] = Bg[x];
+
+    int32_t* Dg = P.ring + (int64_t)g * P.H;
+    int32_t* Dl = reinterpret_cast<int32_t*>(smem + P.bw_max);
+    if (D_LDS) {
+        for (int x = lane; x < P.H; x += 64) Dl[x] = Dg[x];
+    }
+    __syncthreads();
+
+    // steps t < t_lim are simulated in this launch
+    const int64_t want = (int64_t)st.t + P.step_delta;
+    const int t_lim = (int)min(want, (int64_t)P.max_steps + 2);
+
+    const bool stepped = P.stepped[g] != 0;
+    if (D_LDS) {
+        if (stepped) run_stepped(P, sg, B, S, W1, Dl, st, t_lim);
+        else run_known(P, sg, B, S, W1, Dl, st, t_lim);
+    } else {
+        if (stepped) run_stepped(P, sg, B, S, W1, Dg, st, t_lim);
+        else run_known(P, sg, B, S, W1, Dg, st, t_lim);
+    }
+    __syncthreads();
+    for (int x = lane; x < W0 + W1; x += 64) Bg[x] = B[x];
+    if (D_LDS) {
+        for (int x = lane; x < P.H; x += 64) Dg[x] = Dl[x];
+    }
+    if (lane == 0) P.st[g] = st;
+}
+
+// ------------------------------------------------------------ finalize
+
+__global__ __launch_bounds__(64) void k_finalize(FinArgs F) {
+    const int g = blockIdx.x;
+    const int lane = lane_id();
+    const int pol = g / F.I, inst = g - pol * F.I;
+    const int64_t off = F.offsets[inst];
+    const int n = (int)(F.offsets[inst + 1] - off);
+    const int64_t base = (int64_t)pol * F.N + off;
+    const SegState st = F.st[g];
+    const bool stepped = F.stepped[g] != 0;
+    const int t_end = st.t;
+    long long lat = 0, rs = 0, pre = 0;
+    int mk = 0;
+    for (int j = lane; j < n; j += 64) {
+        const int k = F.start[base + j];
+        int f = F.fin[base + j];
+        if (f > t_end - 1) f = -1;
+        F.fin_out[base + j] = f;
+        if (f >= 0) {
+            lat += (long long)f - F.a[off + j];
+            mk = max(mk, f);
+        }
+        if (!stepped && k >= 0) rs += (long long)min(k + F.o[off + j], t_end) - k;
+        pre += F.preempt[base + j];
+    }
+    lat = wave_sum_i64(lat);
+    rs = wave_sum_i64(rs);
+    pre = wave_sum_i64(pre);
+    mk = wave_max_i32(mk);
+    if (lane == 0) {
+        StatsOut so;
+        so.makespan = mk;
+        so.status = st.status;
+        so.sum_latency = lat;
+        so.request_steps = stepped ? st.req_steps : rs;
+        so.peak_mem = st.peak;
+        so.preemptions = pre;
+        so.t_end = t_end;
+        F.stats[g] = so;
+    }
+}
+
+// ------------------------------------------------------------ launchers
+
+static inline int grid_for(int64_t n, int bs) {
+    int64_t g = (n + bs - 1) / bs;
+    if (g > 65536) g = 65536;
+    return (int)(g < 1 ? 1 : g);
+}
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fill_i32, dim3(grid_for(n, 256)), dim3(256), 0, s, p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u64(uint64_t* p, int64_t n, uint64_t v, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fill_u64, dim3(grid_for(n, 256)), dim3(256), 0, s, p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_init_state(SegState* st, int32_t G, hipStream_t s) {
+    if (G <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_init_state, dim3((G + 255) / 256), dim3(256), 0, s, st, G);
+    return hipGetLastError();
+}
+
+hipError_t launch_chunk_sort(const SortArgs& A, int nchunks, hipStream_t s) {
+    if (nchunks <= 0) return hipSuccess;
+    switch (A.CH) {
+    case 64: hipLaunchKernelGGL((k_chunk_sort<64, 64>), dim3(nchunks), dim3(64), 0, s, A); break;
+    case 128: hipLaunchKernelGGL((k_chunk_sort<128, 64>), dim3(nchunks), dim3(64), 0, s, A); break;
+    case 256: hipLaunchKernelGGL((k_chunk_sort<256, 128>), dim3(nchunks), dim3(128), 0, s, A); break;
+    case 512: hipLaunchKernelGGL((k_chunk_sort<512, 256>), dim3(nchunks), dim3(256), 0, s, A); break;
+    case 1024: hipLaunchKernelGGL((k_chunk_sort<1024, 256>), dim3(nchunks), dim3(256), 0, s, A); break;
+    case 2048: hipLaunchKernelGGL((k_chunk_sort<2048, 512>), dim3(nchunks), dim3(512), 0, s, A); break;
+    case 4096: hipLaunchKernelGGL((k_chunk_sort<4096, 512>), dim3(nchunks), dim3(512), 0, s, A); break;
+    case 8192: hipLaunchKernelGGL((k_chunk_sort<8192, 1024>), dim3(nchunks), dim3(1024), 0, s, A); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_merge_pass(const SortArgs& A, int nchunks, int w, hipStream_t s) {
+    if (nchunks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_merge_pass, dim3(nchunks), dim3(256), 0, s, A, w);
+    return hipGetLastError();
+}
+
+hipError_t launch_build_rec(const SortArgs& A, int nchunks, hipStream_t s) {
+    if (nchunks <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_build_rec, dim3(nchunks), dim3(256), 0, s, A);
+    return hipGetLastError();
+}
+
+hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, size_t lds_bytes, hipStream_t s) {
+    if (G <= 0) return hipSuccess;
+    if (d_lds) {
+        hipLaunchKernelGGL((k_sim<true>), dim3(G), dim3(64), lds_bytes, s, P);
+    } else {
+        hipLaunchKernelGGL((k_sim<false>), dim3(G), dim3(64), lds_bytes, s, P);
+    }
+    return hipGetLastError();
+}
+
+hipError_t prepare_sim(bool d_lds, size_t lds_bytes) {
+    if (lds_bytes <= 65536) return hipSuccess;
+    if (d_lds)
+        return hipFuncSetAttribute((const void*)k_sim<true>,
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    return hipFuncSetAttribute((const void*)k_sim<false>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+}
+
+hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s) {
+    if (G <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_finalize, dim3(G), dim3(64), 0, s, F);
+    return hipGetLastError();
+}
+
+}  // namespace svfk

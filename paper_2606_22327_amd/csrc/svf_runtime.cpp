@@ -1,0 +1,600 @@
+// svf_runtime.cpp -- host side of the C ABI declared in include/svfsim.h:
+// validation, buffer ownership, launch configuration, timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "svf_kernels.h"
+#include "svfsim.h"
+
+using svfk::SegState;
+using svfk::StatsOut;
+
+static_assert(sizeof(StatsOut) == sizeof(svf_instance_stats), "stats layout");
+static_assert(sizeof(SegState) == 72, "state layout");
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int ok() { return SVF_OK; }
+
+constexpr int64_t kLimit30 = int64_t(1) << 30;
+
+int64_t next_pow2(int64_t x) {
+    int64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+struct Timed {
+    int kind;  // 0 init, 1 sim, 2 final
+    hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct svf_batch {
+    hipStream_t stream = nullptr;
+    int device = 0;
+    int32_t I = 0, P = 0;
+    int64_t N = 0;
+    int32_t M = 0, O0 = 0, O1 = 0, max_steps = 0;
+    std::vector<int32_t> policies;
+    std::vector<int64_t> offsets;
+    int32_t H = 1, CH = 64, nchunks = 0, bw_max = 0, max_n = 0;
+    int64_t bw_total = 0;
+    bool d_lds = true;
+    size_t lds_bytes = 0;
+    bool any_stepped = false;
+    bool was_reset = false, dirty = false;
+    bool prof = false;
+    std::vector<Timed> timed;
+    double acc_ms[3] = {0, 0, 0};
+    int64_t sim_launches = 0;
+
+    // device buffers
+    int64_t* d_off = nullptr;
+    int32_t *d_a = nullptr, *d_s = nullptr, *d_o = nullptr, *d_plan = nullptr;
+    int8_t* d_bit = nullptr;
+    int32_t* d_pol = nullptr;
+    int32_t *d_chunk_seg = nullptr, *d_chunk_lo = nullptr;
+    uint64_t *d_keys0 = nullptr, *d_keys1 = nullptr;
+    int4* d_rec = nullptr;
+    int32_t* d_rank = nullptr;
+    uint8_t* d_stepped = nullptr;
+    int64_t* d_bw_off = nullptr;
+    uint64_t* d_bitmap = nullptr;
+    int32_t* d_ring = nullptr;
+    int32_t *d_start = nullptr, *d_fin = nullptr, *d_pre = nullptr, *d_seq = nullptr;
+    int32_t *d_act = nullptr, *d_evl = nullptr;
+    SegState* d_st = nullptr;
+    int32_t* d_fin_out = nullptr;
+    StatsOut* d_stats = nullptr;
+    const uint64_t* sorted_keys = nullptr;  // which key buffer holds the final order
+};
+
+namespace {
+
+template <typename T>
+int dalloc(T** p, int64_t count) {
+    *p = nullptr;
+    if (count <= 0) return SVF_OK;
+    hipError_t e = hipMalloc((void**)p, sizeof(T) * (size_t)count);
+    if (e != hipSuccess) {
+        *p = nullptr;
+        return fail(SVF_ENOMEM, "hipMalloc of %lld bytes failed: %s",
+                    (long long)(sizeof(T) * count), hipGetErrorString(e));
+    }
+    return SVF_OK;
+}
+
+void free_all(svf_batch* h) {
+    void* ptrs[] = {h->d_off, h->d_a, h->d_s, h->d_o, h->d_plan, h->d_bit, h->d_pol,
+                    h->d_chunk_seg, h->d_chunk_lo, h->d_keys0, h->d_keys1, h->d_rec,
+                    h->d_rank, h->d_stepped, h->d_bw_off, h->d_bitmap, h->d_ring,
+                    h->d_start, h->d_fin, h->d_pre, h->d_seq, h->d_act, h->d_evl,
+                    h->d_st, h->d_fin_out, h->d_stats};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    for (auto& t : h->timed) {
+        (void)hipEventDestroy(t.a);
+        (void)hipEventDestroy(t.b);
+    }
+    h->timed.clear();
+}
+
+#define HIPCHK(expr)                                                                  \
+    do {                                                                              \
+        hipError_t e_ = (expr);                                                       \
+        if (e_ != hipSuccess)                                                         \
+            return fail(SVF_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));     \
+    } while (0)
+
+#define RETCHK(expr)              \
+    do {                          \
+        int r_ = (expr);          \
+        if (r_ != SVF_OK) return r_; \
+    } while (0)
+
+struct HostView {
+    const int32_t *a, *s, *o, *plan;
+    const int8_t* bit;
+};
+
+// Everything that can be checked without a GPU.
+int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64_t>& off,
+             int64_t N, std::vector<uint8_t>* stepped, int64_t* max_plan) {
+    const int32_t I = d->num_instances, P = d->num_policies;
+    bool has1bit = false;
+    for (int p = 0; p < P; ++p) has1bit |= d->policies[p] == SVF_POLICY_SVF1BIT;
+    if (N > 0 && (!v.a || !v.s || !v.o))
+        return fail(SVF_EINVAL, "arrival, prompt and output must not be NULL");
+    if (has1bit && N > 0 && !v.bit) return fail(SVF_EINVAL, "SVF1BIT needs long_bit");
+    if (has1bit && (d->O0 < 1 || d->O1 < 1)) return fail(SVF_EINVAL, "SVF1BIT needs O0, O1 >= 1");
+    *max_plan = 1;
+    stepped->assign((size_t)P * I, 0);
+    for (int32_t i = 0; i < I; ++i) {
+        const int64_t lo = off[i], hi = off[i + 1];
+        for (int64_t j = lo; j < hi; ++j) {
+            const int32_t a = v.a[j], s = v.s[j], o = v.o[j];
+            if (a < 0 || a >= kLimit30)
+                return fail(SVF_EINVAL, "instance %d request %lld: arrival %d out of [0, 2^30)", i,
+                            (long long)(j - lo), a);
+            if (j > lo && a < v.a[j - 1])
+                return fail(SVF_EINVAL, "instance %d: arrivals not in order at request %lld", i,
+                            (long long)(j - lo));
+            if (s < 1) return fail(SVF_EINVAL, "instance %d request %lld: prompt %d < 1", i, (long long)(j - lo), s);
+            if (o < 1) return fail(SVF_EINVAL, "instance %d request %lld: output %d < 1", i, (long long)(j - lo), o);
+            if (v.plan && v.plan[j] < 1)
+                return fail(SVF_EINVAL, "instance %d request %lld: plan_len %d < 1", i, (long long)(j - lo), v.plan[j]);
+            if (v.bit && v.bit[j] != 0 && v.bit[j] != 1)
+                return fail(SVF_EINVAL, "instance %d request %lld: long_bit %d not 0/1", i, (long long)(j - lo), v.bit[j]);
+            for (int p = 0; p < P; ++p) {
+                const int pol = d->policies[p];
+                int64_t oh;
+                if (pol == SVF_POLICY_SVF1BIT) oh = v.bit[j] ? d->O1 : d->O0;
+                else oh = v.plan ? v.plan[j] : o;
+                if ((int64_t)s + std::max<int64_t>(o, oh) > d->M)
+                    return fail(SVF_EINFEASIBLE,
+                                "instance %d request %lld: s + max(o, planned) = %lld exceeds M = %lld",
+                                i, (long long)(j - lo), (long long)s + std::max<int64_t>(o, oh),
+                                (long long)d->M);
+                uint64_t key;
+                if (pol == SVF_POLICY_FCFS) key = (uint64_t)a;
+                else if (pol == SVF_POLICY_SJF) key = (uint64_t)oh;
+                else key = (uint64_t)s * (uint64_t)oh + (((uint64_t)oh * oh + oh) >> 1);
+                if (key >= (uint64_t(1) << 32))
+                    return fail(SVF_EINVAL, "instance %d request %lld: priority key %llu >= 2^32", i,
+                                (long long)(j - lo), (unsigned long long)key);
+                if (oh != o) (*stepped)[(size_t)p * I + i] = 1;
+                *max_plan = std::max(*max_plan, oh);
+            }
+        }
+    }
+    return SVF_OK;
+}
+
+int check_desc_shape(const svf_batch_desc* d, std::vector<int64_t>* off, int64_t* N) {
+    if (!d) return fail(SVF_EINVAL, "desc is NULL");
+    if (d->num_instances < 0) return fail(SVF_EINVAL, "num_instances < 0");
+    if (!d->req_offsets) return fail(SVF_EINVAL, "req_offsets is NULL");
+    if (d->num_policies < 1 || d->num_policies > 8)
+        return fail(SVF_EINVAL, "num_policies must be in 1..8 (got %d)", d->num_policies);
+    if (!d->policies) return fail(SVF_EINVAL, "policies is NULL");
+    for (int p = 0; p < d->num_policies; ++p)
+        if (d->policies[p] < SVF_POLICY_FCFS || d->policies[p] > SVF_POLICY_SVF1BIT)
+            return fail(SVF_EINVAL, "unknown policy %d", d->policies[p]);
+    if (d->M < 1 || d->M >= kLimit30) return fail(SVF_EINVAL, "M must be in [1, 2^30)");
+    if (d->max_steps < 0 || d->max_steps >= kLimit30)
+        return fail(SVF_EINVAL, "max_steps must be in [0, 2^30)");
+    off->assign(d->req_offsets, d->req_offsets + d->num_instances + 1);
+    if ((*off)[0] != 0) return fail(SVF_EINVAL, "req_offsets[0] must be 0");
+    for (int32_t i = 0; i < d->num_instances; ++i) {
+        const int64_t n = (*off)[i + 1] - (*off)[i];
+        if (n < 0) return fail(SVF_EINVAL, "req_offsets decreases at instance %d", i);
+        if (n >= (int64_t(1) << 31) - 1)
+            return fail(SVF_EINVAL, "instance %d holds too many requests", i);
+    }
+    *N = (*off)[d->num_instances];
+    if (*N * (int64_t)d->num_policies >= (int64_t(1) << 31))
+        return fail(SVF_EINVAL, "requests x policies must stay below 2^31");
+    return SVF_OK;
+}
+
+void record(svf_batch* h, int kind, hipEvent_t* a) {
+    if (!h->prof) return;
+    (void)hipEventCreate(a);
+    (void)hipEventRecord(*a, h->stream);
+    (void)kind;
+}
+
+void record_end(svf_batch* h, int kind, hipEvent_t a) {
+    if (!h->prof) return;
+    hipEvent_t b;
+    (void)hipEventCreate(&b);
+    (void)hipEventRecord(b, h->stream);
+    h->timed.push_back({kind, a, b});
+}
+
+int do_reset(svf_batch* h) {
+    const int32_t G = h->P * h->I;
+    const int64_t PN = (int64_t)h->P * h->N;
+    hipEvent_t e0 = nullptr;
+    record(h, 0, &e0);
+    HIPCHK(svfk::launch_init_state(h->d_st, G, h->stream));
+    HIPCHK(svfk::launch_fill_u64(h->d_bitmap, (int64_t)h->P * h->bw_total, 0ull, h->stream));
+    HIPCHK(svfk::launch_fill_i32(h->d_ring, (int64_t)G * h->H, 0, h->stream));
+    HIPCHK(svfk::launch_fill_i32(h->d_start, PN, -1, h->stream));
+    HIPCHK(svfk::launch_fill_i32(h->d_fin, PN, -1, h->stream));
+    HIPCHK(svfk::launch_fill_i32(h->d_pre, PN, 0, h->stream));
+    HIPCHK(svfk::launch_fill_i32(h->d_seq, PN, -1, h->stream));
+    if (PN > 0) {
+        svfk::SortArgs A{};
+        A.offsets = h->d_off;
+        A.a = h->d_a; A.s = h->d_s; A.o = h->d_o; A.plan = h->d_plan; A.bit = h->d_bit;
+        A.policies = h->d_pol;
+        A.chunk_seg = h->d_chunk_seg;
+        A.chunk_lo = h->d_chunk_lo;
+        A.rec = h->d_rec;
+        A.rank = h->d_rank;
+        A.I = h->I; A.P = h->P; A.N = h->N; A.O0 = h->O0; A.O1 = h->O1; A.CH = h->CH;
+        A.keys_in = nullptr;
+        A.keys_out = h->d_keys0;
+        HIPCHK(svfk::launch_chunk_sort(A, h->nchunks, h->stream));
+        uint64_t* cur = h->d_keys0;
+        uint64_t* other = h->d_keys1;
+        for (int64_t w = h->CH; w < h->max_n; w *= 2) {
+            A.keys_in = cur;
+            A.keys_out = other;
+            HIPCHK(svfk::launch_merge_pass(A, h->nchunks, (int)w, h->stream));
+            std::swap(cur, other);
+        }
+        A.keys_in = cur;
+        A.keys_out = nullptr;
+        HIPCHK(svfk::launch_build_rec(A, h->nchunks, h->stream));
+    }
+    record_end(h, 0, e0);
+    h->was_reset = true;
+    h->dirty = true;
+    return SVF_OK;
+}
+
+int do_sim(svf_batch* h, int64_t delta) {
+    const int32_t G = h->P * h->I;
+    if (G <= 0) return SVF_OK;
+    svfk::SimArgs S{};
+    S.offsets = h->d_off;
+    S.a = h->d_a;
+    S.rec = h->d_rec;
+    S.rank = h->d_rank;
+    S.stepped = h->d_stepped;
+    S.bw_off = h->d_bw_off;
+    S.bitmap = h->d_bitmap;
+    S.ring = h->d_ring;
+    S.start = h->d_start;
+    S.fin = h->d_fin;
+    S.preempt = h->d_pre;
+    S.admit_seq = h->d_seq;
+    S.act = h->d_act;
+    S.evl = h->d_evl;
+    S.st = h->d_st;
+    S.I = h->I; S.P = h->P; S.N = h->N;
+    S.bw_total = h->bw_total;
+    S.bw_max = h->bw_max;
+    S.H = h->H;
+    S.M = h->M;
+    S.max_steps = h->max_steps;
+    S.step_delta = delta;
+    hipEvent_t e0 = nullptr;
+    record(h, 1, &e0);
+    HIPCHK(svfk::launch_sim(S, G, h->d_lds, h->lds_bytes, h->stream));
+    record_end(h, 1, e0);
+    h->sim_launches += 1;
+    h->dirty = true;
+    return SVF_OK;
+}
+
+int do_finalize(svf_batch* h) {
+    if (!h->dirty) return SVF_OK;
+    const int32_t G = h->P * h->I;
+    svfk::FinArgs F{};
+    F.offsets = h->d_off;
+    F.a = h->d_a;
+    F.o = h->d_o;
+    F.stepped = h->d_stepped;
+    F.start = h->d_start;
+    F.fin = h->d_fin;
+    F.preempt = h->d_pre;
+    F.st = h->d_st;
+    F.fin_out = h->d_fin_out;
+    F.stats = h->d_stats;
+    F.I = h->I; F.P = h->P; F.N = h->N;
+    hipEvent_t e0 = nullptr;
+    record(h, 2, &e0);
+    HIPCHK(svfk::launch_finalize(F, G, h->stream));
+    record_end(h, 2, e0);
+    h->dirty = false;
+    return SVF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* svf_last_error(void) { return g_err.c_str(); }
+
+int svf_abi_version(void) { return SVFSIM_ABI_VERSION; }
+
+int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
+    g_err.clear();
+    if (!out) return fail(SVF_EINVAL, "out is NULL");
+    *out = nullptr;
+    std::vector<int64_t> off;
+    int64_t N = 0;
+    RETCHK(check_desc_shape(d, &off, &N));
+    const int32_t I = d->num_instances, P = d->num_policies;
+
+    // host view of the per-request arrays (device inputs are fetched first)
+    std::vector<int32_t> ha, hs, ho, hp;
+    std::vector<int8_t> hb;
+    HostView v{d->arrival, d->prompt, d->output, d->plan_len, d->long_bit};
+    if (d->inputs_on_device && N > 0) {
+        if (!d->arrival || !d->prompt || !d->output)
+            return fail(SVF_EINVAL, "arrival, prompt and output must not be NULL");
+        ha.resize(N); hs.resize(N); ho.resize(N);
+        HIPCHK(hipMemcpy(ha.data(), d->arrival, 4 * N, hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(hs.data(), d->prompt, 4 * N, hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(ho.data(), d->output, 4 * N, hipMemcpyDeviceToHost));
+        v.a = ha.data(); v.s = hs.data(); v.o = ho.data();
+        if (d->plan_len) {
+            hp.resize(N);
+            HIPCHK(hipMemcpy(hp.data(), d->plan_len, 4 * N, hipMemcpyDeviceToHost));
+            v.plan = hp.data();
+        }
+        if (d->long_bit) {
+            hb.resize(N);
+            HIPCHK(hipMemcpy(hb.data(), d->long_bit, N, hipMemcpyDeviceToHost));
+            v.bit = hb.data();
+        }
+    }
+    std::vector<uint8_t> stepped;
+    int64_t max_plan = 1;
+    RETCHK(validate(d, v, off, N, &stepped, &max_plan));
+
+    svf_batch* h = new (std::nothrow) svf_batch();
+    if (!h) return fail(SVF_ENOMEM, "host allocation failed");
+    h->stream = (hipStream_t)hip_stream;
+    (void)hipGetDevice(&h->device);
+    h->I = I; h->P = P; h->N = N;
+    h->M = (int32_t)d->M;
+    h->O0 = d->O0; h->O1 = d->O1;
+    h->max_steps = (int32_t)d->max_steps;
+    h->policies.assign(d->policies, d->policies + P);
+    h->offsets = off;
+    h->H = (int32_t)next_pow2(std::max<int64_t>(max_plan, 1));
+    for (int32_t i = 0; i < I; ++i) h->max_n = std::max<int32_t>(h->max_n, (int32_t)(off[i + 1] - off[i]));
+    h->CH = (int32_t)std::min<int64_t>(8192, std::max<int64_t>(64, next_pow2(h->max_n)));
+    for (uint8_t x : stepped) h->any_stepped |= x != 0;
+
+    // chunk table (segment, first position) and bitmap offsets
+    std::vector<int32_t> cseg, clo;
+    std::vector<int64_t> bw_off(I + 1, 0);
+    for (int32_t i = 0; i < I; ++i) {
+        const int64_t n = off[i + 1] - off[i];
+        const int64_t W0 = (n + 63) / 64, W1 = (W0 + 63) / 64;
+        bw_off[i + 1] = bw_off[i] + W0 + W1;
+        h->bw_max = std::max<int32_t>(h->bw_max, (int32_t)(W0 + W1));
+    }
+    h->bw_total = bw_off[I];
+    for (int32_t p = 0; p < P; ++p)
+        for (int32_t i = 0; i < I; ++i) {
+            const int64_t n = off[i + 1] - off[i];
+            for (int64_t lo = 0; lo < n; lo += h->CH) {
+                cseg.push_back(p * I + i);
+                clo.push_back((int32_t)lo);
+            }
+        }
+    h->nchunks = (int32_t)cseg.size();
+
+    // ring placement: LDS when the ring and bitmap fit comfortably
+    const char* env = getenv("SVFSIM_RING");
+    const size_t ring_bytes = (size_t)h->H * 4;
+    const size_t bm_bytes = (size_t)h->bw_max * 8;
+    h->d_lds = ring_bytes + bm_bytes <= 65536;
+    if (env && !strcmp(env, "global")) h->d_lds = false;
+    if (env && !strcmp(env, "lds") && ring_bytes + bm_bytes <= 160 * 1024) h->d_lds = true;
+    h->lds_bytes = std::max<size_t>(8, bm_bytes + (h->d_lds ? ring_bytes : 0));
+    if (h->lds_bytes > 160 * 1024) {
+        delete h;
+        return fail(SVF_EINVAL, "an instance's rank bitmap needs %zu bytes of LDS (> 160 KB)", h->lds_bytes);
+    }
+
+    const int64_t G = (int64_t)P * I;
+    const int64_t PN = (int64_t)P * N;
+    int rc = SVF_OK;
+#define ALLOC(ptr, cnt) \
+    if (rc == SVF_OK) rc = dalloc(&h->ptr, (cnt));
+    ALLOC(d_off, I + 1);
+    ALLOC(d_a, N);
+    ALLOC(d_s, N);
+    ALLOC(d_o, N);
+    if (d->plan_len) ALLOC(d_plan, N);
+    if (d->long_bit) ALLOC(d_bit, N);
+    ALLOC(d_pol, P);
+    ALLOC(d_chunk_seg, h->nchunks);
+    ALLOC(d_chunk_lo, h->nchunks);
+    ALLOC(d_keys0, PN);
+    ALLOC(d_keys1, PN);
+    ALLOC(d_rec, PN);
+    ALLOC(d_rank, PN);
+    ALLOC(d_stepped, G);
+    ALLOC(d_bw_off, I + 1);
+    ALLOC(d_bitmap, (int64_t)P * h->bw_total);
+    ALLOC(d_ring, G * h->H);
+    ALLOC(d_start, PN);
+    ALLOC(d_fin, PN);
+    ALLOC(d_pre, PN);
+    ALLOC(d_seq, PN);
+    if (h->any_stepped) {
+        ALLOC(d_act, PN);
+        ALLOC(d_evl, PN);
+    }
+    ALLOC(d_st, G);
+    ALLOC(d_fin_out, PN);
+    ALLOC(d_stats, G);
+#undef ALLOC
+    if (rc != SVF_OK) {
+        free_all(h);
+        delete h;
+        return rc;
+    }
+    const hipMemcpyKind kind = d->inputs_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+    hipError_t e = hipSuccess;
+#define CPY(dst, src, bytes, k) \
+    if (e == hipSuccess && (bytes) > 0) e = hipMemcpyAsync((dst), (src), (bytes), (k), h->stream);
+    CPY(h->d_off, off.data(), 8 * (I + 1), hipMemcpyHostToDevice);
+    CPY(h->d_a, d->arrival, 4 * N, kind);
+    CPY(h->d_s, d->prompt, 4 * N, kind);
+    CPY(h->d_o, d->output, 4 * N, kind);
+    if (d->plan_len) CPY(h->d_plan, d->plan_len, 4 * N, kind);
+    if (d->long_bit) CPY(h->d_bit, d->long_bit, N, kind);
+    CPY(h->d_pol, h->policies.data(), 4 * P, hipMemcpyHostToDevice);
+    CPY(h->d_chunk_seg, cseg.data(), 4 * (int64_t)cseg.size(), hipMemcpyHostToDevice);
+    CPY(h->d_chunk_lo, clo.data(), 4 * (int64_t)clo.size(), hipMemcpyHostToDevice);
+    CPY(h->d_stepped, stepped.data(), G, hipMemcpyHostToDevice);
+    CPY(h->d_bw_off, bw_off.data(), 8 * (I + 1), hipMemcpyHostToDevice);
+#undef CPY
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+    if (e == hipSuccess) {
+        hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes);
+        if (a != hipSuccess) e = a;
+    }
+    if (e != hipSuccess) {
+        free_all(h);
+        delete h;
+        return fail(SVF_EHIP, "copying the inputs failed: %s", hipGetErrorString(e));
+    }
+    *out = h;
+    return ok();
+}
+
+int svf_reset(svf_batch* h) {
+    if (!h) return fail(SVF_EINVAL, "handle is NULL");
+    return do_reset(h);
+}
+
+int svf_step(svf_batch* h, int64_t nsteps) {
+    if (!h) return fail(SVF_EINVAL, "handle is NULL");
+    if (nsteps < 0) return fail(SVF_EINVAL, "nsteps < 0");
+    if (!h->was_reset) RETCHK(do_reset(h));
+    // nsteps == 0 still launches: instances that are already complete at their
+    // current step (e.g. empty ones) get their final status
+    return do_sim(h, std::min<int64_t>(nsteps, int64_t(1) << 40));
+}
+
+int svf_run(svf_batch* h) {
+    if (!h) return fail(SVF_EINVAL, "handle is NULL");
+    if (!h->was_reset) RETCHK(do_reset(h));
+    return do_sim(h, int64_t(1) << 40);
+}
+
+int svf_read(svf_batch* h, int32_t slot, int32_t* start, int32_t* finish, int32_t* preempt,
+             int32_t* admit_seq, int32_t outputs_on_device) {
+    if (!h) return fail(SVF_EINVAL, "handle is NULL");
+    if (slot < 0 || slot >= h->P) return fail(SVF_EINVAL, "policy slot %d out of range", slot);
+    if (!h->was_reset) return fail(SVF_ESTATE, "nothing simulated yet (call svf_reset/svf_run)");
+    RETCHK(do_finalize(h));
+    const int64_t base = (int64_t)slot * h->N;
+    const size_t bytes = 4 * (size_t)h->N;
+    const hipMemcpyKind k = outputs_on_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost;
+    if (bytes) {
+        if (start) HIPCHK(hipMemcpyAsync(start, h->d_start + base, bytes, k, h->stream));
+        if (finish) HIPCHK(hipMemcpyAsync(finish, h->d_fin_out + base, bytes, k, h->stream));
+        if (preempt) HIPCHK(hipMemcpyAsync(preempt, h->d_pre + base, bytes, k, h->stream));
+        if (admit_seq) HIPCHK(hipMemcpyAsync(admit_seq, h->d_seq + base, bytes, k, h->stream));
+    }
+    if (!outputs_on_device) HIPCHK(hipStreamSynchronize(h->stream));
+    return ok();
+}
+
+int svf_stats(svf_batch* h, int32_t slot, svf_instance_stats* out) {
+    if (!h) return fail(SVF_EINVAL, "handle is NULL");
+    if (slot < 0 || slot >= h->P) return fail(SVF_EINVAL, "policy slot %d out of range", slot);
+    if (!out && h->I > 0) return fail(SVF_EINVAL, "out is NULL");
+    if (!h->was_reset) return fail(SVF_ESTATE, "nothing simulated yet (call svf_reset/svf_run)");
+    RETCHK(do_finalize(h));
+    if (h->I > 0)
+        HIPCHK(hipMemcpyAsync(out, h->d_stats + (int64_t)slot * h->I,
+                              sizeof(svf_instance_stats) * h->I, hipMemcpyDeviceToHost, h->stream));
+    HIPCHK(hipStreamSynchronize(h->stream));
+    return ok();
+}
+
+int svf_set_profiling(svf_batch* h, int32_t enable) {
+    if (!h) return fail(SVF_EINVAL, "handle is NULL");
+    HIPCHK(hipStreamSynchronize(h->stream));
+    for (auto& t : h->timed) {
+        (void)hipEventDestroy(t.a);
+        (void)hipEventDestroy(t.b);
+    }
+    h->timed.clear();
+    h->acc_ms[0] = h->acc_ms[1] = h->acc_ms[2] = 0;
+    h->sim_launches = 0;
+    h->prof = enable != 0;
+    return ok();
+}
+
+int svf_timings(svf_batch* h, svf_timing* out) {
+    if (!h || !out) return fail(SVF_EINVAL, "NULL argument");
+    HIPCHK(hipStreamSynchronize(h->stream));
+    for (auto& t : h->timed) {
+        float ms = 0;
+        HIPCHK(hipEventElapsedTime(&ms, t.a, t.b));
+        h->acc_ms[t.kind] += ms;
+        (void)hipEventDestroy(t.a);
+        (void)hipEventDestroy(t.b);
+    }
+    h->timed.clear();
+    out->init_ms = h->acc_ms[0];
+    out->sim_ms = h->acc_ms[1];
+    out->final_ms = h->acc_ms[2];
+    out->sim_launches = h->sim_launches;
+    return ok();
+}
+
+int svf_shape(const svf_batch* h, int64_t* num_requests, int32_t* num_instances,
+              int32_t* num_policies) {
+    if (!h) return fail(SVF_EINVAL, "handle is NULL");
+    if (num_requests) *num_requests = h->N;
+    if (num_instances) *num_instances = h->I;
+    if (num_policies) *num_policies = h->P;
+    return ok();
+}
+
+int svf_destroy(svf_batch* h) {
+    if (!h) return ok();
+    (void)hipStreamSynchronize(h->stream);
+    free_all(h);
+    delete h;
+    return ok();
+}
+
+}  // extern "C"

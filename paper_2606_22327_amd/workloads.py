@@ -153,8 +153,11 @@ def default_max_steps(b: Batch) -> int:
 # The configurations
 # --------------------------------------------------------------------------
 
-def gen_instance(cfg: int, inst: int, n: Optional[int] = None) -> Dict[str, np.ndarray]:
-    """Draw one instance of configuration ``cfg`` (per-instance stream)."""
+def gen_instance(cfg: int, inst: int, n: Optional[int] = None,
+                 burst: int = 20000) -> Dict[str, np.ndarray]:
+    """Draw one instance of configuration ``cfg`` (per-instance stream).
+    ``burst`` only applies to the large-queue configuration (reduced copies
+    for tests keep its burst structure with fewer requests per burst)."""
     rng = _rng(cfg if cfg != 3 else 2, inst)
     if cfg == 1:
         # Offline burst, known outputs: 50 requests at t = 0.
@@ -191,7 +194,7 @@ def gen_instance(cfg: int, inst: int, n: Optional[int] = None) -> Dict[str, np.n
     if cfg == 5:
         # Large queues: bursts of 20,000 arrivals every 500 steps.
         n = 200000 if n is None else n
-        a = 500 * (np.arange(n, dtype=np.int64) // 20000)
+        a = 500 * (np.arange(n, dtype=np.int64) // burst)
         s = _uniform(rng, 1, 4096, n)
         o = np.clip(rng.geometric(1.0 / 400.0, size=n), 1, 8192).astype(np.int64)
         return {"arrival": a, "prompt": s, "output": o}
@@ -226,7 +229,7 @@ CONFIG_TITLES = {
 
 
 def config(cfg: int, instances=None, n: Optional[int] = None,
-           policies: Optional[Sequence[str]] = None) -> Batch:
+           policies: Optional[Sequence[str]] = None, burst: int = 20000) -> Batch:
     """Build configuration ``cfg``.
 
     ``instances``: None for the full count, an int for the first k instances,
@@ -242,7 +245,7 @@ def config(cfg: int, instances=None, n: Optional[int] = None,
         ids = range(instances)
     else:
         ids = list(instances)
-    parts = [gen_instance(cfg, int(i), n) for i in ids]
+    parts = [gen_instance(cfg, int(i), n, burst) for i in ids]
     b = assemble(f"cfg{cfg}", parts, spec["M"], tuple(policies or spec["policies"]),
                  O0=spec.get("O0", 0), O1=spec.get("O1", 0),
                  meta={"cfg": cfg, "ids": list(map(int, ids)) if not isinstance(ids, range)

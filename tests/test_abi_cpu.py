@@ -1,0 +1,107 @@
+"""The C-ABI library on the CPU: it loads, exports what the header declares,
+and rejects bad input before touching the GPU (no compute calls here)."""
+
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2606_22327_amd import svfsim as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "svfsim.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(svf_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = S.load()
+    names = declared_functions()
+    assert set(names) == set(S.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", S.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\sT\s(svf_[a-z_]+)$", out, flags=re.M))
+    assert set(names) <= exported
+
+
+def test_abi_version():
+    assert S.abi_version() == 1
+
+
+def _make(**kw):
+    base = dict(offsets=[0, 3], arrival=np.array([0, 1, 1]), prompt=np.array([2, 3, 4]),
+                output=np.array([5, 6, 7]), M=20, policies=["svf"])
+    base.update(kw)
+    return S.Simulator(base.pop("offsets"), base.pop("arrival"), base.pop("prompt"),
+                       base.pop("output"), base.pop("M"), base.pop("policies"), **base)
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(output=np.array([5, 0, 7])), "SVF_EINVAL", "output"),
+    (dict(prompt=np.array([0, 3, 4])), "SVF_EINVAL", "prompt"),
+    (dict(arrival=np.array([2, 1, 1])), "SVF_EINVAL", "order"),
+    (dict(arrival=np.array([-1, 1, 1])), "SVF_EINVAL", "arrival"),
+    (dict(M=10), "SVF_EINFEASIBLE", "exceeds M"),
+    (dict(M=0), "SVF_EINVAL", "M must"),
+    (dict(M=2 ** 30), "SVF_EINVAL", "M must"),
+    (dict(policies=["svf1bit"]), "SVF_EINVAL", "long_bit"),
+    (dict(policies=["svf1bit"], long_bit=np.array([0, 1, 2]), O0=1, O1=2), "SVF_EINVAL", "long_bit"),
+    (dict(policies=["svf1bit"], long_bit=np.array([0, 1, 1]), O0=0, O1=2), "SVF_EINVAL", "O0"),
+    (dict(policies=["svf1bit"], long_bit=np.array([0, 1, 1]), O0=1, O1=30), "SVF_EINFEASIBLE", "planned"),
+    (dict(plan_len=np.array([1, 0, 1])), "SVF_EINVAL", "plan_len"),
+    (dict(plan_len=np.array([1, 40, 1]), M=42), "SVF_EINFEASIBLE", "planned"),
+    (dict(max_steps=-1), "SVF_EINVAL", "max_steps"),
+    (dict(offsets=[1, 3]), "SVF_EINVAL", "req_offsets[0]"),
+    (dict(offsets=[0, 3, 2]), "SVF_EINVAL", "decreases"),
+])
+def test_create_rejects_bad_input(kw, code, text):
+    with pytest.raises(S.SvfError) as ei:
+        _make(**kw)
+    assert ei.value.name == code
+    assert text in str(ei.value)
+    assert text in S.last_error()
+
+
+def test_key_overflow_is_rejected():
+    # volume of s = 65535, o = 65535 exceeds 2^32
+    with pytest.raises(S.SvfError) as ei:
+        _make(prompt=np.array([65535, 1, 1]), output=np.array([65535, 1, 1]), M=2 ** 29)
+    assert ei.value.name == "SVF_EINVAL" and "2^32" in str(ei.value)
+
+
+def test_unknown_policy_and_policy_count():
+    lib = S.load()
+    import ctypes
+    d = S.BatchDesc()
+    off = np.array([0, 0], dtype=np.int64)
+    pol = np.array([7], dtype=np.int32)
+    d.num_instances = 1
+    d.req_offsets = off.ctypes.data
+    d.M = 10
+    d.num_policies = 1
+    d.policies = pol.ctypes.data
+    h = ctypes.c_void_p()
+    assert lib.svf_create(ctypes.byref(d), None, ctypes.byref(h)) == -1
+    assert b"unknown policy" in lib.svf_last_error()
+    d.num_policies = 0
+    assert lib.svf_create(ctypes.byref(d), None, ctypes.byref(h)) == -1
+    assert lib.svf_create(None, None, ctypes.byref(h)) == -1
+    assert lib.svf_create(ctypes.byref(d), None, None) == -1
+
+
+def test_null_handle_calls():
+    lib = S.load()
+    assert lib.svf_destroy(None) == 0
+    for fn, args in (("svf_reset", ()), ("svf_run", ()), ("svf_step", (1,)),
+                     ("svf_set_profiling", (1,))):
+        assert getattr(lib, fn)(None, *args) == -1
+    assert lib.svf_read(None, 0, None, None, None, None, 0) == -1
+    assert lib.svf_stats(None, 0, None) == -1

@@ -1,0 +1,334 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Every integer output is compared element by element (start, finish,
+preemption count, admission order) together with the per-instance
+statistics.  Small cases run the oracle on every instance; the full-size
+configurations, in the launch configuration the benchmark times, are compared
+on sampled instances (each instance is independent and regenerated from its
+own seed) and checked on all instances through properties that hold at any
+size.
+"""
+
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import validate
+from paper_2606_22327_amd import svfsim as S
+from paper_2606_22327_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+FIELDS = ("start", "finish", "preempt", "admit_seq")
+SFIELDS = ("makespan", "status", "sum_latency", "request_steps", "peak_mem", "preemptions",
+           "t_end")
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+THREADS = min(16, os.cpu_count() or 1)
+
+
+def say(msg):
+    print(f"[gpu-parity] {msg}", file=sys.stderr, flush=True)
+
+
+def gpu_run(batch, policies=None, device_inputs=False, chunks=None):
+    """Run on the GPU; ``chunks``: list of svf_step sizes instead of one run."""
+    pols = tuple(policies or batch.policies)
+    sim = S.Simulator.from_batch(batch, pols, device_inputs=device_inputs)
+    try:
+        if chunks is None:
+            sim.run()
+        else:
+            for c in chunks:
+                sim.step(c)
+        out = {}
+        for slot, pol in enumerate(pols):
+            d = sim.read(slot)
+            d["stats"] = sim.stats(slot)
+            out[pol] = d
+    finally:
+        sim.close()
+    return out
+
+
+def compare(batch, g, pol, ids=None, t_stop=2 ** 62, max_steps=None, label=""):
+    """Oracle on the listed instances (all by default) vs the GPU outputs."""
+    ids = list(range(batch.num_instances)) if ids is None else list(ids)
+    sub = batch.subset(ids) if len(ids) != batch.num_instances else batch
+    r = oracle.run(sub, pol, threads=THREADS, t_stop=t_stop, max_steps=max_steps)
+    for j, i in enumerate(ids):
+        glo, ghi = int(batch.offsets[i]), int(batch.offsets[i + 1])
+        olo, ohi = int(sub.offsets[j]), int(sub.offsets[j + 1])
+        for f in FIELDS:
+            a = g[f][glo:ghi]
+            b = r[f][olo:ohi]
+            if not np.array_equal(a, b):
+                k = int(np.nonzero(a != b)[0][0])
+                raise AssertionError(f"{label} {pol} instance {i} field {f}: first mismatch at "
+                                     f"request {k}: gpu {int(a[k])} oracle {int(b[k])}")
+        for c, f in enumerate(oracle.STAT_FIELDS):
+            if f not in SFIELDS:
+                continue
+            gv = int(g["stats"][f][i])
+            ov = int(r["stats"][j, c])
+            assert gv == ov, f"{label} {pol} instance {i} stat {f}: gpu {gv} oracle {ov}"
+
+
+def properties(batch, g, pol, ids=None):
+    """Checks that hold at any size for known-length runs: V1, V2 and the
+    statistics recomputed from the schedule."""
+    ids = range(batch.num_instances) if ids is None else ids
+    for i in ids:
+        lo, hi = int(batch.offsets[i]), int(batch.offsets[i + 1])
+        a = batch.arrival[lo:hi].astype(np.int64)
+        s = batch.prompt[lo:hi].astype(np.int64)
+        o = batch.output[lo:hi].astype(np.int64)
+        k = g["start"][lo:hi].astype(np.int64)
+        f = g["finish"][lo:hi].astype(np.int64)
+        st = g["stats"][i]
+        assert int(st["status"]) == 0
+        assert (k >= a).all() and (f == k + o).all()
+        prof = validate.true_profile(s, o, k, int(f.max()) + 1 if hi > lo else 1)
+        assert int(prof.max()) <= batch.M
+        assert int(st["peak_mem"]) == int(prof.max())
+        assert int(st["makespan"]) == (int(f.max()) if hi > lo else 0)
+        assert int(st["sum_latency"]) == int((f - a).sum())
+        assert int(st["request_steps"]) == int(o.sum())
+        assert int(st["preemptions"]) == 0
+        seq = g["admit_seq"][lo:hi].astype(np.int64)
+        assert np.array_equal(np.sort(seq), np.arange(hi - lo))
+        assert (np.diff(k[np.argsort(seq, kind="stable")]) >= 0).all()
+
+
+# ------------------------------------------------------------ small, full oracle
+
+def test_config1_full():
+    b = W.config(1)
+    say("config 1: 256 x 50, fcfs/sjf/svf")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="cfg1")
+
+
+def test_config2_subset():
+    b = W.config(2, instances=64)
+    say("config 2: 64 x 1000")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="cfg2")
+
+
+def test_config3_subset_with_onebit_and_preemption():
+    b = W.config(3, instances=64)
+    say("config 3: 64 x 1000, 1-bit with preemption")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="cfg3")
+    assert int(g["svf1bit"]["stats"]["preemptions"].sum()) > 0
+
+
+def test_config4_subset():
+    b = W.config(4, instances=16)
+    say("config 4: 16 x 5000")
+    g = gpu_run(b)
+    compare(b, g["svf"], "svf", label="cfg4")
+
+
+def test_config5_reduced_bursts():
+    b = W.config(5, instances=3, n=6000, burst=1500)
+    say("config 5 reduced: 3 x 6000 in bursts of 1500 (sort with merge passes: no)")
+    g = gpu_run(b)
+    compare(b, g["svf"], "svf", label="cfg5r")
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_ragged(seed):
+    say(f"random ragged batches seed {seed}")
+    for kw in (dict(), dict(bits=True), dict(plan_noise=True)):
+        b = W.random_small(seed, instances=40, n_max=60, s_max=12, o_max=20, M=60,
+                           gap_mean=[0.0, 0.3, 1.0][seed % 3], **kw)
+        g = gpu_run(b)
+        for pol in b.policies:
+            compare(b, g[pol], pol, label=f"rand{seed}{kw}")
+
+
+def test_ragged_sizes_with_merge_passes():
+    """Instances of very different sizes in one batch: 0, 1, a partial chunk,
+    and several chunks of the 8192-element LDS sort joined by merge passes."""
+    sizes = [0, 1, 70, 9000, 20000, 3]
+    parts = []
+    rng = np.random.default_rng(42)
+    for n in sizes:
+        a = np.floor(np.cumsum(rng.exponential(0.7, n))).astype(np.int64)
+        parts.append({"arrival": a, "prompt": rng.integers(1, 200, n),
+                      "output": rng.integers(1, 300, n)})
+    b = W.assemble("ragged", parts, 4096, ("svf", "sjf", "fcfs"))
+    say("ragged sizes with merge passes")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="ragged")
+
+
+def test_degenerate_cases():
+    say("degenerate cases")
+    # all instances empty
+    e = W.assemble("empty", [{"arrival": [], "prompt": [], "output": []}] * 5, 10, ("svf",))
+    g = gpu_run(e)
+    assert g["svf"]["stats"]["t_end"].tolist() == [0] * 5
+    # one request; exact fit s + o = M; equal keys; unbounded memory
+    parts = [
+        {"arrival": np.array([3]), "prompt": np.array([7]), "output": np.array([9])},
+        {"arrival": np.zeros(20), "prompt": np.full(20, 4), "output": np.full(20, 12)},
+        {"arrival": np.arange(30) // 3, "prompt": np.full(30, 1), "output": np.full(30, 1)},
+    ]
+    b = W.assemble("deg", parts, 16, ("svf", "sjf", "fcfs"))
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="deg")
+    big = W.config(2, instances=4, n=300)
+    b2 = W.assemble("big", [big.instance(i) for i in range(4)], 2 ** 29 // 4,
+                    ("svf", "sjf", "fcfs"))
+    g = gpu_run(b2)
+    for pol in b2.policies:
+        compare(b2, g[pol], pol, label="unbounded")
+        assert np.array_equal(g[pol]["start"], b2.arrival)
+
+
+def test_step_by_step_equals_run_and_partial_states():
+    b = W.random_small(11, instances=24, n_max=50, s_max=10, o_max=16, M=40, gap_mean=0.5,
+                       bits=True)
+    say("svf_step chunks vs one run, and vs the oracle stopped at the same step")
+    full = gpu_run(b)
+    T = max(int(full[p]["stats"]["t_end"].max()) for p in b.policies)
+    ones = min(T, 3000)
+    one = gpu_run(b, chunks=[1] * ones + [T])
+    for pol in b.policies:
+        for f in FIELDS:
+            assert np.array_equal(full[pol][f], one[pol][f]), (pol, f)
+        assert np.array_equal(full[pol]["stats"], one[pol]["stats"]), pol
+    for stop in (0, 1, 5, 17, 60, 333):
+        g = gpu_run(b, chunks=[stop] if stop else [0])
+        for pol in b.policies:
+            compare(b, g[pol], pol, t_stop=stop, label=f"t_stop={stop}")
+    g = gpu_run(b, chunks=[7, 3, 11, 10 ** 9])
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="chunks")
+    # known lengths only: the event-driven path across many small launches
+    b2 = W.config(2, instances=16, n=300)
+    full = gpu_run(b2)
+    T = max(int(full[p]["stats"]["t_end"].max()) for p in b2.policies)
+    parts = gpu_run(b2, chunks=[1] * 200 + [13] * 50 + [T])
+    for pol in b2.policies:
+        for f in FIELDS:
+            assert np.array_equal(full[pol][f], parts[pol][f]), (pol, f)
+        assert np.array_equal(full[pol]["stats"], parts[pol]["stats"]), pol
+        for stop in (150, 777):
+            g = gpu_run(b2, chunks=[stop])
+            compare(b2, g[pol], pol, t_stop=stop, label=f"known t_stop={stop}")
+
+
+def test_step_budget_exhaustion():
+    b = W.config(2, instances=8, n=400)
+    b.max_steps = 150
+    say("max_steps exhaustion")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, max_steps=150, label="exhausted")
+        assert (g[pol]["stats"]["status"] == 1).all()
+    b3 = W.config(3, instances=8, n=400)
+    b3.max_steps = 200
+    g = gpu_run(b3)
+    for pol in b3.policies:
+        compare(b3, g[pol], pol, max_steps=200, label="exhausted3")
+
+
+def test_device_inputs_and_determinism():
+    import torch
+    b = W.config(3, instances=32)
+    say("device inputs + determinism")
+    g1 = gpu_run(b)
+    g2 = gpu_run(b, device_inputs=True)
+    for pol in b.policies:
+        for f in FIELDS:
+            assert np.array_equal(g1[pol][f], g2[pol][f])
+        assert np.array_equal(g1[pol]["stats"], g2[pol]["stats"])
+    sim = S.Simulator.from_batch(b)
+    sim.run()
+    a = sim.read(0)
+    sim.reset()
+    sim.run()
+    c = sim.read(0)
+    n = sim.num_requests
+    dev = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in range(4)]
+    sim.read_device(0, *dev)
+    torch.cuda.synchronize()
+    sim.close()
+    for f in FIELDS:
+        assert np.array_equal(a[f], c[f])
+    for f, t in zip(FIELDS, dev):
+        assert np.array_equal(a[f], t.cpu().numpy())
+
+
+# ------------------------------------------------ full sizes, sampled
+
+def _sample(n_inst, k, seed):
+    rng = np.random.default_rng(seed)
+    ids = sorted(set([0, n_inst - 1] + rng.choice(n_inst, size=k, replace=False).tolist()))
+    return ids
+
+
+def test_full_config2_sampled():
+    b = W.config(2)
+    say("full config 2: 4096 x 1000 x 3 policies")
+    t0 = time.time()
+    g = gpu_run(b)
+    say(f"  gpu done in {time.time() - t0:.1f}s; comparing samples")
+    for pol in b.policies:
+        compare(b, g[pol], pol, ids=_sample(b.num_instances, 30, 2), label="cfg2full")
+        assert (g[pol]["stats"]["status"] == 0).all()
+        assert (g[pol]["stats"]["preemptions"] == 0).all()
+        properties(b, g[pol], pol, ids=_sample(b.num_instances, 200, 7))
+
+
+def test_full_config3_sampled():
+    b = W.config(3)
+    say("full config 3: 4096 x 1000 x 4 policies")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, ids=_sample(b.num_instances, 30, 3), label="cfg3full")
+        assert (g[pol]["stats"]["status"] == 0).all()
+
+
+def test_full_config4_sampled():
+    b = W.config(4)
+    say("full config 4: 16384 x 5000")
+    t0 = time.time()
+    g = gpu_run(b)
+    say(f"  gpu done in {time.time() - t0:.1f}s; comparing samples")
+    compare(b, g["svf"], "svf", ids=_sample(b.num_instances, 20, 4), label="cfg4full")
+    assert (g["svf"]["stats"]["status"] == 0).all()
+    properties(b, g["svf"], "svf", ids=_sample(b.num_instances, 60, 5))
+
+
+def test_full_config5_against_stored_oracle_digests():
+    path = os.path.join(GOLDEN, "oracle_digests.json")
+    data = json.load(open(path))["cfg5/svf"]
+    b = W.config(5)
+    assert b.max_steps == data["max_steps"]
+    say("full config 5: 64 x 200000")
+    g = gpu_run(b)["svf"]
+    for i_str, ent in data["instances"].items():
+        i = int(i_str)
+        lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+        h = hashlib.sha256()
+        for f in FIELDS:
+            h.update(np.ascontiguousarray(g[f][lo:hi], dtype=np.int32).tobytes())
+        assert h.hexdigest() == ent["sha256_start_finish_preempt_admit"], f"instance {i}"
+        for f in SFIELDS:
+            assert int(g["stats"][f][i]) == ent["stats"][f], (i, f)
+    properties(b, g, "svf")
