@@ -241,6 +241,73 @@ struct Seg {
     int32_t* __restrict__ evl;
 };
 
+// Order LDS accesses of different lanes of this wave.  LDS executes one
+// wave's instructions in issue order, so only the compiler has to be stopped
+// from moving accesses across this point.
+__device__ __forceinline__ void lds_order() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+}
+
+// Wave-wide reductions with DPP inside rows of 16 lanes, then four readlanes.
+// Must be called with every lane active.
+__device__ __forceinline__ int row_max_dpp(int v) {
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false));  // row_half_mirror
+    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false));  // row_mirror
+    return v;
+}
+
+__device__ __forceinline__ int row_min_dpp(int v) {
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false));
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false));
+    return v;
+}
+
+__device__ __forceinline__ int wmax(int v) {
+    const int r = row_max_dpp(v);
+    return max(max(__builtin_amdgcn_readlane(r, 0), __builtin_amdgcn_readlane(r, 16)),
+               max(__builtin_amdgcn_readlane(r, 32), __builtin_amdgcn_readlane(r, 48)));
+}
+
+__device__ __forceinline__ int wmin(int v) {
+    const int r = row_min_dpp(v);
+    return min(min(__builtin_amdgcn_readlane(r, 0), __builtin_amdgcn_readlane(r, 16)),
+               min(__builtin_amdgcn_readlane(r, 32), __builtin_amdgcn_readlane(r, 48)));
+}
+
+__device__ __forceinline__ int4 readlane4(const int4& v, int src) {
+    int4 r;
+    r.x = __builtin_amdgcn_readlane(v.x, src);
+    r.y = __builtin_amdgcn_readlane(v.y, src);
+    r.z = __builtin_amdgcn_readlane(v.z, src);
+    r.w = __builtin_amdgcn_readlane(v.w, src);
+    return r;
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int src) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), src);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// The future memory profile, in LDS (ordered by issue) or in global memory
+// (ordered with a workgroup barrier, which also waits for outstanding stores).
+template <bool LDS>
+struct Ring {
+    int32_t* p;
+    int mask;
+    __device__ __forceinline__ int ld(int tau) const { return p[tau & mask]; }
+    __device__ __forceinline__ void st(int tau, int v) const { p[tau & mask] = v; }
+    __device__ __forceinline__ static void order() {
+        if (LDS) lds_order(); else __syncthreads();
+    }
+};
+
 // Lowest set bit of the two-level rank bitmap, or -1.
 __device__ __forceinline__ int bitmap_first(const uint64_t* B, const uint64_t* S, int W1) {
     const int lane = lane_id();
@@ -249,7 +316,7 @@ __device__ __forceinline__ int bitmap_first(const uint64_t* B, const uint64_t* S
         const uint64_t m = ballot(v != 0ull);
         if (m) {
             const int f = __builtin_ctzll(m);
-            const uint64_t sv = __shfl(v, f);
+            const uint64_t sv = readlane64(v, f);
             const int w = (base + f) * 64 + __builtin_ctzll(sv);
             const uint64_t bw = B[w];
             return w * 64 + __builtin_ctzll(bw);
@@ -272,140 +339,213 @@ __device__ __forceinline__ void bitmap_clear(uint64_t* B, uint64_t* S, int r) {
     if (nb == 0ull) S[w >> 6] &= ~(1ull << (w & 63));
 }
 
-// Arrivals at step t: the requests [cursor, ...) with a == t form a prefix
-// (arrivals are sorted).  Sets their rank bits; returns the smallest new rank.
-__device__ __forceinline__ int ingest_arrivals(const Seg& sg, uint64_t* B, uint64_t* S, int t,
-                                               int& cursor) {
-    const int lane = lane_id();
-    int min_rank = INT32_MAX;
-    while (cursor < sg.n) {
-        const int i = cursor + lane;
-        const bool arr = (i < sg.n) && (sg.a[i] == t);
-        const uint64_t m = ballot(arr);
-        if (m == 0ull) break;
-        int r = INT32_MAX;
-        if (arr) {
-            r = sg.rank[i];
-            if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
-            else r = INT32_MAX;
-        }
-        min_rank = min(min_rank, wave_min_i32(r));
-        const int cnt = __popcll(m);
-        cursor += cnt;
-        if (cnt < 64) break;
-    }
-    wave_sync();
-    return min_rank;
-}
-
-// Forward-looking check of a candidate (size s_h, planned length oh) at step t.
-// extra1 is added at tau = t+1 (requests running past their plan).  Returns
-// true if it fits; otherwise *t_free receives the first step at which every
-// violation seen in this window has disappeared (valid while D is unchanged).
-template <typename DPtr>
-__device__ __forceinline__ bool check_fit(DPtr D, int Hm, int t, int s_h, int oh, int M,
-                                          int64_t extra1, int* t_free) {
+// Forward-looking check of a candidate (size s_h, planned length oh) started
+// at step t, fused with its admission: every future step tau = t+1+j,
+// j < oh, must satisfy D[tau] + (s_h + j + 1) (+ extra1 at j = 0) <= M.
+// If it fits, the candidate's growth is added to D and true is returned.
+// Otherwise *t_free receives the first step at which every violation seen has
+// disappeared while D stays unchanged (tau leaves the window, or the candidate
+// would start late enough: t' >= D[tau] + tau + s_h - M).
+// Loads are issued four per lane at a time; the first 256 steps of the window
+// stay in registers between the check and the update.
+template <bool LDS>
+__device__ __forceinline__ bool fit_and_admit(Ring<LDS> D, int t, int s_h, int oh, int M,
+                                              int extra1, int* t_free) {
     const int lane = lane_id();
     const int X = M - s_h;
     bool viol = false;
     int rel = INT32_MIN;
-    for (int j = lane; j < oh; j += 64) {
-        const int tau = t + 1 + j;
-        int64_t v = (int64_t)D[tau & Hm] + (j + 1);
-        if (j == 0) v += extra1;
-        if (v > X) {
+    int d0[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int j = lane + 64 * u;
+        d0[u] = j < oh ? D.ld(t + 1 + j) : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int j = lane + 64 * u;
+        const int v = d0[u] + j + 1 + (j == 0 ? extra1 : 0);
+        if (j < oh && v > X) {
             viol = true;
-            const int64_t r = (int64_t)t + (v - X);
-            rel = max(rel, (int)min((int64_t)tau, r));
+            rel = max(rel, min(t + 1 + j, t + (v - X)));
         }
     }
-    const bool fits = ballot(viol) == 0ull;
-    if (!fits) *t_free = wave_max_i32(rel);
-    return fits;
-}
-
-template <typename DPtr>
-__device__ __forceinline__ void add_growth(DPtr D, int Hm, int t, int s_h, int oh) {
-    for (int j = lane_id(); j < oh; j += 64) D[(t + 1 + j) & Hm] += s_h + j + 1;
+    for (int base = 256; base < oh; base += 256) {
+        int d[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int j = base + lane + 64 * u;
+            d[u] = j < oh ? D.ld(t + 1 + j) : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int j = base + lane + 64 * u;
+            const int v = d[u] + j + 1;
+            if (j < oh && v > X) {
+                viol = true;
+                rel = max(rel, min(t + 1 + j, t + (v - X)));
+            }
+        }
+    }
+    if (ballot(viol) != 0ull) {
+        *t_free = wmax(rel);
+        return false;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int j = lane + 64 * u;
+        if (j < oh) D.st(t + 1 + j, d0[u] + s_h + j + 1);
+    }
+    for (int base = 256; base < oh; base += 256) {
+        int d[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int j = base + lane + 64 * u;
+            d[u] = j < oh ? D.ld(t + 1 + j) : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int j = base + lane + 64 * u;
+            if (j < oh) D.st(t + 1 + j, d[u] + s_h + j + 1);
+        }
+    }
+    Ring<LDS>::order();
+    return true;
 }
 
 // remove the planned profile of a request started at k with planned length L
 // for the future steps tau in [t+1, k+L]
-template <typename DPtr>
-__device__ __forceinline__ void remove_future(DPtr D, int Hm, int t, int s, int k, int L) {
+template <bool LDS>
+__device__ __forceinline__ void remove_future(Ring<LDS> D, int t, int s, int k, int L) {
     const int cnt = k + L - t;
     for (int j = lane_id(); j < cnt; j += 64) {
         const int tau = t + 1 + j;
-        D[tau & Hm] -= s + (tau - k);
+        D.st(tau, D.ld(tau) - (s + (tau - k)));
     }
+    Ring<LDS>::order();
 }
 
 // fold the final steps [t+1, t+len] into the peak and clear them
-template <typename DPtr>
-__device__ __forceinline__ int fold_past(DPtr D, int Hm, int t, int len) {
+template <bool LDS>
+__device__ __forceinline__ int fold_past(Ring<LDS> D, int t, int len) {
     int pm = 0;
     for (int j = lane_id(); j < len; j += 64) {
-        const int slot = (t + 1 + j) & Hm;
-        pm = max(pm, (int)D[slot]);
-        D[slot] = 0;
+        const int tau = t + 1 + j;
+        pm = max(pm, D.ld(tau));
+        D.st(tau, 0);
     }
-    return wave_max_i32(pm);
+    Ring<LDS>::order();
+    return wmax(pm);
 }
 
 // ---- known lengths: event-driven
 
-template <typename DPtr>
+template <bool LDS>
 __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
-                          DPtr D, SegState& st, int t_lim) {
+                          Ring<LDS> D, SegState& st, int t_lim) {
     const int lane = lane_id();
-    const int Hm = P.H - 1;
     const int M = P.M;
+    const int n = sg.n;
     int t = st.t, cursor = st.cursor, seq = st.seq, nadm = st.nfin, max_fin = st.max_fin;
     int head = st.head_rank, t_f = st.t_f;
-    int64_t peak = st.peak;
+    int peak = (int)st.peak;
     int status = STATUS_RUNNING;
+
+    // Arrival window: lane l holds request wb + l (arrival, rank, record).
+    int wb = 0, a_reg = INT32_MAX, rk_reg = 0;
+    int4 aq = make_int4(0, 0, 0, 0);
+    auto load_arrivals = [&](int base) {
+        wb = base;
+        const int i = base + lane;
+        a_reg = INT32_MAX;
+        rk_reg = 0;
+        if (i < n) {
+            a_reg = sg.a[i];
+            rk_reg = sg.rank[i];
+            if ((unsigned)rk_reg >= (unsigned)n) rk_reg = 0;  // only a broken sort
+            aq = sg.rec[rk_reg];
+        }
+    };
+    load_arrivals(cursor);
+
+    // Rank window: lane l holds the record of rank rwb + l.
+    int rwb = INT32_MIN / 2;
+    int4 rw = make_int4(0, 0, 0, 0);
+    auto rec_of = [&](int r) -> int4 {
+        if (r < rwb || r >= rwb + 64) {
+            rwb = r;
+            const int i = r + lane;
+            rw = i < n ? sg.rec[i] : make_int4(0, 0, 0, 0);
+        }
+        return readlane4(rw, r - rwb);
+    };
+    int4 hq = make_int4(0, 0, 0, 0);  // record of the blocked head
+    if (head >= 0) hq = rec_of(head);
+
     for (;;) {
         // every request finished by step t-1 (an empty instance is done at t = 0)
-        if (nadm == sg.n && (nadm == 0 || max_fin <= t - 1)) { status = STATUS_DONE; break; }
+        if (nadm == n && (nadm == 0 || max_fin <= t - 1)) { status = STATUS_DONE; break; }
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
         if (t >= t_lim) break;
-        // 1. arrivals
-        const int new_min = ingest_arrivals(sg, B, S, t, cursor);
+
+        // 1. arrivals: a prefix of the window (arrivals are sorted)
+        int new_min = INT32_MAX;
+        int4 nq = make_int4(0, 0, 0, 0);
+        for (;;) {
+            const bool arr = (wb + lane >= cursor) && (a_reg == t);
+            const uint64_t m = ballot(arr);
+            if (m == 0ull) break;
+            if (arr) bitmap_set_atomic(B, S, rk_reg);
+            const int mn = wmin(arr ? rk_reg : INT32_MAX);
+            if (mn < new_min) {
+                new_min = mn;
+                const int src = __builtin_ctzll(ballot(arr && rk_reg == mn));
+                nq = readlane4(aq, src);
+            }
+            cursor += __popcll(m);
+            if (cursor < wb + 64) break;
+            load_arrivals(cursor);
+        }
+        lds_order();
+
         // 4. admissions (known lengths: completions change nothing ahead)
-        if (head < 0 || new_min < head || t >= t_f) {
+        // (head < 0 means nothing was waiting before this step's arrivals)
+        const int head_eff = head < 0 ? INT32_MAX : head;
+        if (new_min < head_eff || (head >= 0 && t >= t_f)) {
+            int r = head;
+            int4 q = hq;
+            if (new_min < head_eff) { r = new_min; q = nq; }
             for (;;) {
-                const int r = bitmap_first(B, S, W1);
-                if (r < 0) { head = -1; break; }
-                const int4 q = sg.rec[r];
                 int tf = 0;
-                if (!check_fit(D, Hm, t, q.y, q.z, M, 0, &tf)) { head = r; t_f = tf; break; }
-                add_growth(D, Hm, t, q.y, q.z);
+                if (!fit_and_admit(D, t, q.y, q.z, M, 0, &tf)) { head = r; hq = q; t_f = tf; break; }
                 if (lane == 0) {
                     bitmap_clear(B, S, r);
                     sg.start[q.x] = t;
                     sg.admit_seq[q.x] = seq;
                     sg.fin[q.x] = t + q.w;
                 }
-                wave_sync();
+                lds_order();
                 ++seq;
                 ++nadm;
                 max_fin = max(max_fin, t + q.w);
+                r = bitmap_first(B, S, W1);
+                if (r < 0) { head = -1; break; }
+                q = rec_of(r);
             }
         }
+
         // 5. advance to the next step where anything can happen
+        const int next_arr = cursor < wb + 64 ? __builtin_amdgcn_readlane(a_reg, cursor - wb)
+                                              : (cursor < n ? sg.a[cursor] : INT32_MAX);
         int nt;
-        const int next_arr = cursor < sg.n ? sg.a[cursor] : INT32_MAX;
         if (head >= 0) nt = min(t_f, next_arr);
-        else if (cursor < sg.n) nt = next_arr;
+        else if (cursor < n) nt = next_arr;
         else nt = max_fin + 1;
         nt = max(nt, t + 1);
         nt = min(nt, t_lim);
         nt = min(nt, P.max_steps + 1);
         if (nt <= t) nt = t + 1;
-        const int len = min(nt - t, P.H);
-        const int pm = fold_past(D, Hm, t, len);
-        wave_sync();
-        peak = max(peak, (int64_t)pm);
+        peak = max(peak, fold_past(D, t, min(nt - t, P.H)));
         t = nt;
     }
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nadm; st.max_fin = max_fin;
@@ -414,11 +554,10 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
 
 // ---- planned lengths differ from the truth: one step at a time
 
-template <typename DPtr>
+template <bool LDS>
 __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
-                            DPtr D, SegState& st, int t_lim) {
+                            Ring<LDS> D, SegState& st, int t_lim) {
     const int lane = lane_id();
-    const int Hm = P.H - 1;
     const int M = P.M;
     int t = st.t, cursor = st.cursor, seq = st.seq, nfin = st.nfin, nA = st.nA, N_O = st.N_O;
     int64_t C_O = st.C_O, peak = st.peak, req_steps = st.req_steps;
@@ -428,7 +567,20 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
         if (t >= t_lim) break;
         // 1. arrivals
-        ingest_arrivals(sg, B, S, t, cursor);
+        while (cursor < sg.n) {
+            const int i = cursor + lane;
+            const bool arr = (i < sg.n) && (sg.a[i] == t);
+            const uint64_t m = ballot(arr);
+            if (m == 0ull) break;
+            if (arr) {
+                const int r = sg.rank[i];
+                if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
+            }
+            const int cnt = __popcll(m);
+            cursor += cnt;
+            if (cnt < 64) break;
+        }
+        lds_order();
         // 2. completions and requests reaching their planned length
         {
             int newA = 0;
@@ -458,17 +610,18 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                 while (early) {
                     const int src = __builtin_ctzll(early);
                     early &= early - 1;
-                    const int ks = bcast_i32(k, src), ss = bcast_i32(s, src), ls = bcast_i32(oh, src);
-                    remove_future(D, Hm, t, ss, ks, ls);
+                    remove_future(D, t, __builtin_amdgcn_readlane(s, src),
+                                  __builtin_amdgcn_readlane(k, src),
+                                  __builtin_amdgcn_readlane(oh, src));
                 }
                 const uint64_t keep = ballot(live && !done);
                 dfin += __popcll(ballot(done));
                 // in-place compaction: every kept entry moves to a lower or equal slot
                 const int pos = newA + __popcll(keep & ((1ull << lane) - 1ull));
-                wave_sync();
+                __syncthreads();
                 if (live && !done) sg.act[pos] = r;
                 newA += __popcll(keep);
-                wave_sync();
+                __syncthreads();
             }
             nA = newA;
             C_O += wave_sum_i64(dC);
@@ -479,7 +632,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         //    remaining volume (latest arrival on ties)
         int nev = 0;
         {
-            int64_t mem_next = (int64_t)D[(t + 1) & Hm] + C_O + (int64_t)N_O * (t + 1);
+            int64_t mem_next = (int64_t)D.ld(t + 1) + C_O + (int64_t)N_O * (t + 1);
             while (mem_next > M && nA > 0) {
                 long long bestR = -1;
                 int bestIdx = -1, bestPos = -1;
@@ -492,18 +645,17 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                     if (R > bestR || (R == bestR && q.x > bestIdx)) { bestR = R; bestIdx = q.x; bestPos = x; }
                 }
                 const long long gR = wave_max_i64(bestR);
-                const int gIdx = wave_max_i32(bestR == gR ? bestIdx : -1);
+                const int gIdx = wmax(bestR == gR ? bestIdx : -1);
                 const uint64_t who = ballot(bestR == gR && bestIdx == gIdx);
                 const int src = __builtin_ctzll(who);
-                const int vpos = bcast_i32(bestPos, src);
+                const int vpos = __builtin_amdgcn_readlane(bestPos, src);
                 const int vr = sg.act[vpos];
                 const int4 q = sg.rec[vr];
                 const int k = sg.start[q.x];
                 const int e = t - k;
-                if (e < q.z) remove_future(D, Hm, t, q.y, k, q.z);
+                if (e < q.z) remove_future(D, t, q.y, k, q.z);
                 else { C_O -= (int64_t)(q.y - k); N_O -= 1; }
-                mem_next -= (int64_t)q.y + (t + 1) - k;
-                wave_sync();
+                __syncthreads();
                 if (lane == 0) {
                     sg.act[vpos] = sg.act[nA - 1];
                     sg.preempt[q.x] += 1;
@@ -511,11 +663,10 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                     sg.admit_seq[q.x] = -1;
                     sg.evl[nev] = vr;
                 }
-                wave_sync();
+                __syncthreads();
                 --nA;
                 ++nev;
-                // the ring entry at t+1 may have changed: recompute from parts
-                mem_next = (int64_t)D[(t + 1) & Hm] + C_O + (int64_t)N_O * (t + 1);
+                mem_next = (int64_t)D.ld(t + 1) + C_O + (int64_t)N_O * (t + 1);
             }
         }
         // 4. admissions
@@ -525,15 +676,15 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             const int4 q = sg.rec[r];
             int tf = 0;
             const int64_t extra1 = C_O + (int64_t)N_O * (t + 1);
-            if (!check_fit(D, Hm, t, q.y, q.z, M, extra1, &tf)) break;
-            add_growth(D, Hm, t, q.y, q.z);
+            // extra1 <= M here (step 3 ran), so it fits in int
+            if (!fit_and_admit(D, t, q.y, q.z, M, (int)extra1, &tf)) break;
             if (lane == 0) {
                 bitmap_clear(B, S, r);
                 sg.start[q.x] = t;
                 sg.admit_seq[q.x] = seq;
                 sg.act[nA] = r;
             }
-            wave_sync();
+            __syncthreads();
             ++seq;
             ++nA;
         }
@@ -542,15 +693,14 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             const int r = sg.evl[x];
             if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
         }
-        wave_sync();
+        __syncthreads();
         // 5. advance
         req_steps += nA;
-        const int slot = (t + 1) & Hm;
-        const int64_t mem = (int64_t)D[slot] + C_O + (int64_t)N_O * (t + 1);
+        const int64_t mem = (int64_t)D.ld(t + 1) + C_O + (int64_t)N_O * (t + 1);
         peak = max(peak, mem);
-        wave_sync();
-        if (lane == 0) D[slot] = 0;
-        wave_sync();
+        Ring<LDS>::order();
+        if (lane == 0) D.st(t + 1, 0);
+        Ring<LDS>::order();
         ++t;
     }
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nfin; st.nA = nA; st.N_O = N_O;
@@ -601,14 +751,11 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     const int64_t want = (int64_t)st.t + P.step_delta;
     const int t_lim = (int)min(want, (int64_t)P.max_steps + 2);
 
-    const bool stepped = P.stepped[g] != 0;
-    if (D_LDS) {
-        if (stepped) run_stepped(P, sg, B, S, W1, Dl, st, t_lim);
-        else run_known(P, sg, B, S, W1, Dl, st, t_lim);
-    } else {
-        if (stepped) run_stepped(P, sg, B, S, W1, Dg, st, t_lim);
-        else run_known(P, sg, B, S, W1, Dg, st, t_lim);
-    }
+    Ring<D_LDS> D;
+    D.p = D_LDS ? Dl : Dg;
+    D.mask = P.H - 1;
+    if (P.stepped[g] != 0) run_stepped(P, sg, B, S, W1, D, st, t_lim);
+    else run_known(P, sg, B, S, W1, D, st, t_lim);
     __syncthreads();
     for (int x = lane; x < W0 + W1; x += 64) Bg[x] = B[x];
     if (D_LDS) {
