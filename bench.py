@@ -31,17 +31,27 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def kernel_source_digest():
+    import hashlib
+    src = os.path.join(ROOT, "paper_2606_22327_amd", "csrc", "svf_kernels.hip")
+    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+
+
 def traffic_from_profile(workload):
-    """HBM bytes per sim launch measured by rocprofv3 counters, if recorded for
-    this kernel and workload (profiles/traffic_<workload>.json)."""
+    """HBM bytes per simulation launch measured with rocprofv3 counters
+    (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy kernel's reading),
+    if recorded for this workload and for the current kernel source; None
+    otherwise (profiles/traffic_<workload>.json)."""
     p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(p):
         return None
     try:
         d = json.load(open(p))
-        return d.get("bytes_per_launch")
     except Exception:
         return None
+    if d.get("kernel_source_sha256_16") != kernel_source_digest():
+        return None
+    return d.get("bytes_per_launch")
 
 
 def cpu_baseline(cfg, sample_instances, threads):
@@ -67,8 +77,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--instances", type=int, default=None)
-    ap.add_argument("--cpu-sample", type=int, default=256)
+    ap.add_argument("--cpu-sample", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="after the timed steps, copy MIB MiB device-to-device three times "
+                         "(a plain copy kernel of known size for scaling HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU only; instances are "
@@ -107,6 +120,16 @@ def main():
     wall = time.perf_counter() - t0
     tm = sim.timings()
     log(f"timed {args.steps} steps in {wall:.3f}s; kernel ms: {tm}")
+
+    if args.calibrate_copy:
+        nbytes = args.calibrate_copy << 20
+        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 3 x {nbytes} bytes read and written")
+        del src, dst
 
     # results of the last step
     req_steps = 0
