@@ -67,7 +67,7 @@ struct SimArgs {
     const uint8_t* stepped;   // [G] 1: planned lengths differ from the truth
     const int64_t* bw_off;    // [I+1] bitmap word offset of each instance
     uint64_t* bitmap;         // [P*bw_total]
-    int32_t* ring;            // [G*H]
+    int32_t* ring;            // [G*H] future profile plus step index (G = D + tau)
     int32_t* start;           // [P*N]
     int32_t* fin;
     int32_t* preempt;
@@ -102,6 +102,7 @@ struct FinArgs {
 
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_fill_u64(uint64_t* p, int64_t n, uint64_t v, hipStream_t s);
+hipError_t launch_init_ring(int32_t* ring, int64_t n, int32_t H, hipStream_t s);
 hipError_t launch_init_state(SegState* st, int32_t G, hipStream_t s);
 hipError_t launch_chunk_sort(const SortArgs& A, int nchunks, hipStream_t s);
 hipError_t launch_merge_pass(const SortArgs& A, int nchunks, int w, hipStream_t s);

@@ -115,6 +115,15 @@ __global__ void k_fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
         p[i] = v;
 }
 
+// A fresh ring represents the window [1, H] with D = 0: G[slot] = tau.
+__global__ void k_init_ring(int32_t* __restrict__ ring, int64_t n, int32_t H) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t s = (int32_t)(i & (H - 1));
+        ring[i] = s == 0 ? H : s;
+    }
+}
+
 __global__ void k_init_state(SegState* __restrict__ st, int32_t G) {
     int g = blockIdx.x * blockDim.x + threadIdx.x;
     if (g >= G) return;
@@ -295,16 +304,35 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int src) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-// The future memory profile, in LDS (ordered by issue) or in global memory
-// (ordered with a workgroup barrier, which also waits for outstanding stores).
+// The future memory profile.  Slot tau mod H holds G[tau] = D[tau] + tau,
+// where D[tau] is the memory the running requests are planned to hold at
+// future step tau (a request started at k with planned length L contributes
+// s + (tau - k) for tau in [k+1, k+L]; Section 3.1, eq:c2).  Storing D + tau
+// turns the forward-looking check of a candidate (size s_h) started at t into
+// a plain maximum: every tau in its window needs D[tau] + s_h + (tau - t) <= M,
+// i.e. max G <= (M - s_h) + t.  A slot always represents the one tau of the
+// current window [t+1, t+H] congruent to it; when that step becomes past the
+// slot is rewritten as G = tau' for the next tau' it will represent (D = 0).
+// In LDS, one wave's accesses are ordered by issue; in global memory a
+// workgroup barrier (which also waits for outstanding stores) orders them.
 template <bool LDS>
 struct Ring {
     int32_t* p;
+    int H;
     int mask;
     __device__ __forceinline__ int ld(int tau) const { return p[tau & mask]; }
     __device__ __forceinline__ void st(int tau, int v) const { p[tau & mask] = v; }
     __device__ __forceinline__ static void order() {
         if (LDS) lds_order(); else __syncthreads();
+    }
+    // Visit the window [t+1, t+len] (len <= H) as at most two runs of
+    // consecutive slots: op(first slot, run length, tau of the first slot).
+    template <class Op>
+    __device__ __forceinline__ void runs(int t, int len, Op op) const {
+        const int s0 = (t + 1) & mask;
+        const int L1 = min(len, H - s0);
+        op(s0, L1, t + 1);
+        if (len > L1) op(0, len - L1, t + 1 + L1);
     }
 };
 
@@ -339,116 +367,111 @@ __device__ __forceinline__ void bitmap_clear(uint64_t* B, uint64_t* S, int r) {
     if (nb == 0ull) S[w >> 6] &= ~(1ull << (w & 63));
 }
 
-// Forward-looking check of a candidate (size s_h, planned length oh) started
-// at step t, fused with its admission: every future step tau = t+1+j,
-// j < oh, must satisfy D[tau] + (s_h + j + 1) (+ extra1 at j = 0) <= M.
-// If it fits, the candidate's growth is added to D and true is returned.
-// Otherwise *t_free receives the first step at which every violation seen has
-// disappeared while D stays unchanged (tau leaves the window, or the candidate
-// would start late enough: t' >= D[tau] + tau + s_h - M).
-// Loads are issued four per lane at a time; the first 256 steps of the window
-// stay in registers between the check and the update.
+// Largest G over the window [t+1, t+len], per lane (INT32_MIN if empty).
 template <bool LDS>
-__device__ __forceinline__ bool fit_and_admit(Ring<LDS> D, int t, int s_h, int oh, int M,
-                                              int extra1, int* t_free) {
+__device__ __forceinline__ int window_max(const Ring<LDS>& R, int t, int len) {
     const int lane = lane_id();
+    int m = INT32_MIN;
+    R.runs(t, len, [&](int s, int L, int) {
+        int j = lane;
+        for (; j + 192 < L; j += 256) {
+            const int32_t* q = R.p + s + j;
+            m = max(m, max(max(q[0], q[64]), max(q[128], q[192])));
+        }
+        for (; j < L; j += 64) m = max(m, R.p[s + j]);
+    });
+    return m;
+}
+
+// Add c0 + SLOPE * tau (SLOPE = +1 or -1) to every slot of the window
+// [t+1, t+len].
+template <int SLOPE, bool LDS>
+__device__ __forceinline__ void window_add_linear(const Ring<LDS>& R, int t, int len, int c0) {
+    const int lane = lane_id();
+    R.runs(t, len, [&](int s, int L, int tau0) {
+        int j = lane;
+        int c = c0 + SLOPE * (tau0 + lane);
+        for (; j + 192 < L; j += 256, c += SLOPE * 256) {
+            int32_t* q = R.p + s + j;
+            const int x0 = q[0], x1 = q[64], x2 = q[128], x3 = q[192];
+            q[0] = x0 + c;
+            q[64] = x1 + c + SLOPE * 64;
+            q[128] = x2 + c + SLOPE * 128;
+            q[192] = x3 + c + SLOPE * 192;
+        }
+        for (; j < L; j += 64, c += SLOPE * 64) R.p[s + j] += c;
+    });
+    Ring<LDS>::order();
+}
+
+// Forward-looking check of a candidate (size s_h, planned length oh) started
+// at step t, and its admission when it fits.  extra1 is memory held at t+1
+// only (requests past their planned length).  If the candidate fits, its
+// growth s_h + (tau - t) is added over its window and true is returned.
+// Otherwise *t_free receives the first step at which every violation has
+// disappeared while the profile stays unchanged: a violation at tau persists
+// while tau is still ahead and the start is earlier than G[tau] - (M - s_h);
+// the bound max_tau min(tau, G[tau] - X) is taken over the whole window
+// (steps that do not violate contribute at most t).
+template <bool LDS>
+__device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h, int oh, int M,
+                                              int extra1, int* t_free) {
     const int X = M - s_h;
-    bool viol = false;
-    int rel = INT32_MIN;
-    int d0[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int j = lane + 64 * u;
-        d0[u] = j < oh ? D.ld(t + 1 + j) : 0;
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int j = lane + 64 * u;
-        const int v = d0[u] + j + 1 + (j == 0 ? extra1 : 0);
-        if (j < oh && v > X) {
-            viol = true;
-            rel = max(rel, min(t + 1 + j, t + (v - X)));
-        }
-    }
-    for (int base = 256; base < oh; base += 256) {
-        int d[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int j = base + lane + 64 * u;
-            d[u] = j < oh ? D.ld(t + 1 + j) : 0;
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int j = base + lane + 64 * u;
-            const int v = d[u] + j + 1;
-            if (j < oh && v > X) {
-                viol = true;
-                rel = max(rel, min(t + 1 + j, t + (v - X)));
+    const int lim = X + t;
+    int m = window_max(R, t, oh);
+    if (extra1 != 0) m = max(m, R.ld(t + 1) + extra1);
+    if (ballot(m > lim) != 0ull) {
+        const int lane = lane_id();
+        int rel = INT32_MIN;
+        R.runs(t, oh, [&](int s, int L, int tau0) {
+            for (int j = lane; j < L; j += 64) {
+                const int tau = tau0 + j;
+                const int g = R.p[s + j] + (tau == t + 1 ? extra1 : 0);
+                rel = max(rel, min(tau, g - X));
             }
-        }
-    }
-    if (ballot(viol) != 0ull) {
+        });
         *t_free = wmax(rel);
         return false;
     }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-        const int j = lane + 64 * u;
-        if (j < oh) D.st(t + 1 + j, d0[u] + s_h + j + 1);
-    }
-    for (int base = 256; base < oh; base += 256) {
-        int d[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int j = base + lane + 64 * u;
-            d[u] = j < oh ? D.ld(t + 1 + j) : 0;
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int j = base + lane + 64 * u;
-            if (j < oh) D.st(t + 1 + j, d[u] + s_h + j + 1);
-        }
-    }
-    Ring<LDS>::order();
+    window_add_linear<1>(R, t, oh, s_h - t);
     return true;
 }
 
-// remove the planned profile of a request started at k with planned length L
-// for the future steps tau in [t+1, k+L]
+// Remove the planned profile of a request started at k with planned length L
+// for the future steps tau in [t+1, k+L].
 template <bool LDS>
-__device__ __forceinline__ void remove_future(Ring<LDS> D, int t, int s, int k, int L) {
-    const int cnt = k + L - t;
-    for (int j = lane_id(); j < cnt; j += 64) {
-        const int tau = t + 1 + j;
-        D.st(tau, D.ld(tau) - (s + (tau - k)));
-    }
-    Ring<LDS>::order();
+__device__ __forceinline__ void remove_future(const Ring<LDS>& R, int t, int s, int k, int L) {
+    window_add_linear<-1>(R, t, k + L - t, k - s);
 }
 
-// fold the final steps [t+1, t+len] into the peak and clear them
+// Steps [t+1, t+len] (len = min(nt - t, H)) become past on the way to step nt:
+// fold their memory into the per-lane peak and re-label their slots for the
+// window [nt+1, nt+H].
 template <bool LDS>
-__device__ __forceinline__ int fold_past(Ring<LDS> D, int t, int len) {
-    int pm = 0;
-    for (int j = lane_id(); j < len; j += 64) {
-        const int tau = t + 1 + j;
-        pm = max(pm, D.ld(tau));
-        D.st(tau, 0);
-    }
+__device__ __forceinline__ void fold_past(const Ring<LDS>& R, int t, int nt, int& peak_lane) {
+    const int lane = lane_id();
+    const int len = min(nt - t, R.H);
+    R.runs(t, len, [&](int s, int L, int tau0) {
+        for (int j = lane; j < L; j += 64) {
+            const int tau = tau0 + j;
+            peak_lane = max(peak_lane, R.p[s + j] - tau);
+            R.p[s + j] = nt + 1 + ((tau - nt - 1) & R.mask);
+        }
+    });
     Ring<LDS>::order();
-    return wmax(pm);
 }
 
 // ---- known lengths: event-driven
 
 template <bool LDS>
 __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
-                          Ring<LDS> D, SegState& st, int t_lim) {
+                          const Ring<LDS>& D, SegState& st, int t_lim) {
     const int lane = lane_id();
     const int M = P.M;
     const int n = sg.n;
     int t = st.t, cursor = st.cursor, seq = st.seq, nadm = st.nfin, max_fin = st.max_fin;
     int head = st.head_rank, t_f = st.t_f;
-    int peak = (int)st.peak;
+    int peak_lane = 0;
     int status = STATUS_RUNNING;
 
     // Arrival window: lane l holds request wb + l (arrival, rank, record).
@@ -545,23 +568,26 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         nt = min(nt, t_lim);
         nt = min(nt, P.max_steps + 1);
         if (nt <= t) nt = t + 1;
-        peak = max(peak, fold_past(D, t, min(nt - t, P.H)));
+        fold_past(D, t, nt, peak_lane);
         t = nt;
     }
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nadm; st.max_fin = max_fin;
-    st.head_rank = head; st.t_f = t_f; st.peak = peak; st.status = status;
+    st.head_rank = head; st.t_f = t_f; st.status = status;
+    st.peak = max(st.peak, (int64_t)wmax(peak_lane));
 }
 
 // ---- planned lengths differ from the truth: one step at a time
 
 template <bool LDS>
 __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
-                            Ring<LDS> D, SegState& st, int t_lim) {
+                            const Ring<LDS>& D, SegState& st, int t_lim) {
     const int lane = lane_id();
     const int M = P.M;
     int t = st.t, cursor = st.cursor, seq = st.seq, nfin = st.nfin, nA = st.nA, N_O = st.N_O;
     int64_t C_O = st.C_O, peak = st.peak, req_steps = st.req_steps;
     int status = STATUS_RUNNING;
+    // memory planned for step t+1 by requests within their planned length
+    auto planned_next = [&]() -> int64_t { return (int64_t)D.ld(t + 1) - (t + 1); };
     for (;;) {
         if (nfin == sg.n) { status = STATUS_DONE; break; }
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
@@ -632,7 +658,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         //    remaining volume (latest arrival on ties)
         int nev = 0;
         {
-            int64_t mem_next = (int64_t)D.ld(t + 1) + C_O + (int64_t)N_O * (t + 1);
+            int64_t mem_next = planned_next() + C_O + (int64_t)N_O * (t + 1);
             while (mem_next > M && nA > 0) {
                 long long bestR = -1;
                 int bestIdx = -1, bestPos = -1;
@@ -666,7 +692,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                 __syncthreads();
                 --nA;
                 ++nev;
-                mem_next = (int64_t)D.ld(t + 1) + C_O + (int64_t)N_O * (t + 1);
+                mem_next = planned_next() + C_O + (int64_t)N_O * (t + 1);
             }
         }
         // 4. admissions
@@ -675,9 +701,9 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             if (r < 0) break;
             const int4 q = sg.rec[r];
             int tf = 0;
-            const int64_t extra1 = C_O + (int64_t)N_O * (t + 1);
-            // extra1 <= M here (step 3 ran), so it fits in int
-            if (!fit_and_admit(D, t, q.y, q.z, M, (int)extra1, &tf)) break;
+            // memory of requests past their plan at t+1; <= M after step 3
+            const int extra1 = (int)(C_O + (int64_t)N_O * (t + 1));
+            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, &tf)) break;
             if (lane == 0) {
                 bitmap_clear(B, S, r);
                 sg.start[q.x] = t;
@@ -696,10 +722,10 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         __syncthreads();
         // 5. advance
         req_steps += nA;
-        const int64_t mem = (int64_t)D.ld(t + 1) + C_O + (int64_t)N_O * (t + 1);
+        const int64_t mem = planned_next() + C_O + (int64_t)N_O * (t + 1);
         peak = max(peak, mem);
         Ring<LDS>::order();
-        if (lane == 0) D.st(t + 1, 0);
+        if (lane == 0) D.st(t + 1, t + 1 + D.H);
         Ring<LDS>::order();
         ++t;
     }
@@ -753,6 +779,7 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
 
     Ring<D_LDS> D;
     D.p = D_LDS ? Dl : Dg;
+    D.H = P.H;
     D.mask = P.H - 1;
     if (P.stepped[g] != 0) run_stepped(P, sg, B, S, W1, D, st, t_lim);
     else run_known(P, sg, B, S, W1, D, st, t_lim);
@@ -824,6 +851,12 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
 hipError_t launch_fill_u64(uint64_t* p, int64_t n, uint64_t v, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_fill_u64, dim3(grid_for(n, 256)), dim3(256), 0, s, p, n, v);
+    return hipGetLastError();
+}
+
+hipError_t launch_init_ring(int32_t* ring, int64_t n, int32_t H, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(k_init_ring, dim3(grid_for(n, 256)), dim3(256), 0, s, ring, n, H);
     return hipGetLastError();
 }
 

@@ -241,7 +241,7 @@ int do_reset(svf_batch* h) {
     record(h, 0, &e0);
     HIPCHK(svfk::launch_init_state(h->d_st, G, h->stream));
     HIPCHK(svfk::launch_fill_u64(h->d_bitmap, (int64_t)h->P * h->bw_total, 0ull, h->stream));
-    HIPCHK(svfk::launch_fill_i32(h->d_ring, (int64_t)G * h->H, 0, h->stream));
+    HIPCHK(svfk::launch_init_ring(h->d_ring, (int64_t)G * h->H, h->H, h->stream));
     HIPCHK(svfk::launch_fill_i32(h->d_start, PN, -1, h->stream));
     HIPCHK(svfk::launch_fill_i32(h->d_fin, PN, -1, h->stream));
     HIPCHK(svfk::launch_fill_i32(h->d_pre, PN, 0, h->stream));
@@ -393,6 +393,12 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     for (int32_t i = 0; i < I; ++i) h->max_n = std::max<int32_t>(h->max_n, (int32_t)(off[i + 1] - off[i]));
     h->CH = (int32_t)std::min<int64_t>(8192, std::max<int64_t>(64, next_pow2(h->max_n)));
     for (uint8_t x : stepped) h->any_stepped |= x != 0;
+    // the profile ring stores memory + step index in int32
+    if ((int64_t)h->M + h->max_steps + 2 * (int64_t)h->H >= (int64_t(1) << 31) - 1) {
+        delete h;
+        return fail(SVF_EINVAL, "M + max_steps + 2 * (longest planned length, rounded up to a power "
+                                "of two) must stay below 2^31");
+    }
 
     // chunk table (segment, first position) and bitmap offsets
     std::vector<int32_t> cseg, clo;
