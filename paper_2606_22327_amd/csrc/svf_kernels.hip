@@ -259,34 +259,33 @@ __device__ __forceinline__ void lds_order() {
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 }
 
-// Wave-wide reductions with DPP inside rows of 16 lanes, then four readlanes.
-// Must be called with every lane active.
-__device__ __forceinline__ int row_max_dpp(int v) {
-    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
-    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
-    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false));  // row_half_mirror
-    v = max(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false));  // row_mirror
-    return v;
-}
+// Values the whole wave agrees on, kept in scalar registers.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-__device__ __forceinline__ int row_min_dpp(int v) {
-    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));
-    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));
-    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false));
-    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false));
-    return v;
-}
+// Wave-wide max/min with DPP: within quads, half rows and rows, then the
+// row broadcasts of lanes 15 and 31; lane 63 ends with the result.  Must be
+// called with every lane active.
+#define SVF_DPP_STEP(OP, v, ctrl, rmask) \
+    v = OP(v, __builtin_amdgcn_update_dpp(v, v, ctrl, rmask, 0xF, false))
 
 __device__ __forceinline__ int wmax(int v) {
-    const int r = row_max_dpp(v);
-    return max(max(__builtin_amdgcn_readlane(r, 0), __builtin_amdgcn_readlane(r, 16)),
-               max(__builtin_amdgcn_readlane(r, 32), __builtin_amdgcn_readlane(r, 48)));
+    SVF_DPP_STEP(max, v, 0xB1, 0xF);   // quad_perm 1,0,3,2
+    SVF_DPP_STEP(max, v, 0x4E, 0xF);   // quad_perm 2,3,0,1
+    SVF_DPP_STEP(max, v, 0x141, 0xF);  // row_half_mirror
+    SVF_DPP_STEP(max, v, 0x140, 0xF);  // row_mirror
+    SVF_DPP_STEP(max, v, 0x142, 0xA);  // row_bcast:15 into rows 1 and 3
+    SVF_DPP_STEP(max, v, 0x143, 0xC);  // row_bcast:31 into rows 2 and 3
+    return __builtin_amdgcn_readlane(v, 63);
 }
 
 __device__ __forceinline__ int wmin(int v) {
-    const int r = row_min_dpp(v);
-    return min(min(__builtin_amdgcn_readlane(r, 0), __builtin_amdgcn_readlane(r, 16)),
-               min(__builtin_amdgcn_readlane(r, 32), __builtin_amdgcn_readlane(r, 48)));
+    SVF_DPP_STEP(min, v, 0xB1, 0xF);
+    SVF_DPP_STEP(min, v, 0x4E, 0xF);
+    SVF_DPP_STEP(min, v, 0x141, 0xF);
+    SVF_DPP_STEP(min, v, 0x140, 0xF);
+    SVF_DPP_STEP(min, v, 0x142, 0xA);
+    SVF_DPP_STEP(min, v, 0x143, 0xC);
+    return __builtin_amdgcn_readlane(v, 63);
 }
 
 __device__ __forceinline__ int4 readlane4(const int4& v, int src) {
@@ -347,7 +346,9 @@ __device__ __forceinline__ int bitmap_first(const uint64_t* B, const uint64_t* S
             const uint64_t sv = readlane64(v, f);
             const int w = (base + f) * 64 + __builtin_ctzll(sv);
             const uint64_t bw = B[w];
-            return w * 64 + __builtin_ctzll(bw);
+            const uint32_t lo = (uint32_t)uni((int)(uint32_t)bw);
+            const uint32_t hi = (uint32_t)uni((int)(uint32_t)(bw >> 32));
+            return w * 64 + __builtin_ctzll(((uint64_t)hi << 32) | lo);
         }
     }
     return -1;
@@ -368,17 +369,21 @@ __device__ __forceinline__ void bitmap_clear(uint64_t* B, uint64_t* S, int r) {
 }
 
 // Largest G over the window [t+1, t+len], per lane (INT32_MIN if empty).
+// Runs are walked in uniform blocks of 256 slots (four per lane, two paired
+// LDS reads), then a predicated tail.
 template <bool LDS>
 __device__ __forceinline__ int window_max(const Ring<LDS>& R, int t, int len) {
     const int lane = lane_id();
     int m = INT32_MIN;
     R.runs(t, len, [&](int s, int L, int) {
-        int j = lane;
-        for (; j + 192 < L; j += 256) {
-            const int32_t* q = R.p + s + j;
+        const int32_t* q = R.p + s + lane;
+        const int nb = L >> 8;
+        for (int b = 0; b < nb; ++b, q += 256)
             m = max(m, max(max(q[0], q[64]), max(q[128], q[192])));
-        }
-        for (; j < L; j += 64) m = max(m, R.p[s + j]);
+        const int rem = L & 255;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (lane + 64 * u < rem) m = max(m, q[64 * u]);
     });
     return m;
 }
@@ -389,47 +394,121 @@ template <int SLOPE, bool LDS>
 __device__ __forceinline__ void window_add_linear(const Ring<LDS>& R, int t, int len, int c0) {
     const int lane = lane_id();
     R.runs(t, len, [&](int s, int L, int tau0) {
-        int j = lane;
+        int32_t* q = R.p + s + lane;
         int c = c0 + SLOPE * (tau0 + lane);
-        for (; j + 192 < L; j += 256, c += SLOPE * 256) {
-            int32_t* q = R.p + s + j;
+        int b = 0;
+        for (; b + 1024 <= L; b += 1024, q += 1024, c += SLOPE * 1024) {
+            int x[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) x[u] = q[64 * u];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) q[64 * u] = x[u] + c + SLOPE * 64 * u;
+        }
+        for (; b + 256 <= L; b += 256, q += 256, c += SLOPE * 256) {
             const int x0 = q[0], x1 = q[64], x2 = q[128], x3 = q[192];
             q[0] = x0 + c;
             q[64] = x1 + c + SLOPE * 64;
             q[128] = x2 + c + SLOPE * 128;
             q[192] = x3 + c + SLOPE * 192;
         }
-        for (; j < L; j += 64, c += SLOPE * 64) R.p[s + j] += c;
+        const int rem = L - b;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (lane + 64 * u < rem) q[64 * u] += c + SLOPE * 64 * u;
     });
     Ring<LDS>::order();
 }
 
 // Forward-looking check of a candidate (size s_h, planned length oh) started
 // at step t, and its admission when it fits.  extra1 is memory held at t+1
-// only (requests past their planned length).  If the candidate fits, its
-// growth s_h + (tau - t) is added over its window and true is returned.
-// Otherwise *t_free receives the first step at which every violation has
-// disappeared while the profile stays unchanged: a violation at tau persists
-// while tau is still ahead and the start is earlier than G[tau] - (M - s_h);
-// the bound max_tau min(tau, G[tau] - X) is taken over the whole window
-// (steps that do not violate contribute at most t).
+// only (requests past their planned length).  maxF is a step after which no
+// running request is planned to hold memory (D = 0 there, so the candidate
+// alone, s_h + oh <= M, always fits); the check stops there.  If the
+// candidate fits, its growth s_h + (tau - t) is added over its whole window
+// and true is returned.  Otherwise *t_free receives the first step at which
+// every violation has disappeared while the profile stays unchanged: a
+// violation at tau persists while tau is ahead and the start is earlier than
+// G[tau] - (M - s_h); max_tau min(tau, G[tau] - X) over the window is that
+// step (steps that do not violate contribute at most t).
+// Windows of at most 512 steps take one LDS round trip: eight loads per lane
+// in flight, the values kept in registers for the update.
 template <bool LDS>
 __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h, int oh, int M,
-                                              int extra1, int* t_free) {
+                                              int extra1, int maxF, int* t_free) {
+    const int lane = lane_id();
     const int X = M - s_h;
     const int lim = X + t;
-    int m = window_max(R, t, oh);
-    if (extra1 != 0) m = max(m, R.ld(t + 1) + extra1);
-    if (ballot(m > lim) != 0ull) {
-        const int lane = lane_id();
-        int rel = INT32_MIN;
-        R.runs(t, oh, [&](int s, int L, int tau0) {
-            for (int j = lane; j < L; j += 64) {
-                const int tau = tau0 + j;
-                const int g = R.p[s + j] + (tau == t + 1 ? extra1 : 0);
-                rel = max(rel, min(tau, g - X));
+    int len = max(0, min(oh, maxF - t));
+    if (extra1 != 0) len = max(len, 1);  // step t+1 always carries extra1
+    if (oh <= 512) {
+        int g[8];
+        int m = INT32_MIN, rel = INT32_MIN;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = lane + 64 * u;
+            const int tau = t + 1 + j;
+            g[u] = j < len ? R.ld(tau) : tau;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = lane + 64 * u;
+            const int tau = t + 1 + j;
+            if (j < len) {
+                const int v = g[u] + (j == 0 ? extra1 : 0);
+                m = max(m, v);
+                rel = max(rel, min(tau, v - X));
             }
-        });
+        }
+        if (ballot(m > lim) != 0ull) {
+            *t_free = wmax(rel);
+            return false;
+        }
+        const int c = s_h - t;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int j = lane + 64 * u;
+            const int tau = t + 1 + j;
+            if (j < oh) R.st(tau, g[u] + c + tau);
+        }
+        Ring<LDS>::order();
+        return true;
+    }
+    int m = INT32_MIN, rel = INT32_MIN;
+    R.runs(t, len, [&](int s, int L, int tau0) {
+        const int32_t* q = R.p + s + lane;
+        int tau = tau0 + lane;
+        int b = 0;
+        for (; b + 1024 <= L; b += 1024, q += 1024, tau += 1024) {
+            int x[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) x[u] = q[64 * u];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                m = max(m, x[u]);
+                rel = max(rel, min(tau + 64 * u, x[u] - X));
+            }
+        }
+        for (; b + 256 <= L; b += 256, q += 256, tau += 256) {
+            const int x0 = q[0], x1 = q[64], x2 = q[128], x3 = q[192];
+            m = max(m, max(max(x0, x1), max(x2, x3)));
+            rel = max(rel, max(max(min(tau, x0 - X), min(tau + 64, x1 - X)),
+                               max(min(tau + 128, x2 - X), min(tau + 192, x3 - X))));
+        }
+        const int rem = L - b;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (lane + 64 * u < rem) {
+                const int x = q[64 * u];
+                m = max(m, x);
+                rel = max(rel, min(tau + 64 * u, x - X));
+            }
+    });
+    if (extra1 != 0) {
+        const int v = R.ld(t + 1) + extra1;
+        m = max(m, v);
+        rel = max(rel, min(t + 1, v - X));
+    }
+    if (ballot(m > lim) != 0ull) {
         *t_free = wmax(rel);
         return false;
     }
@@ -444,21 +523,31 @@ __device__ __forceinline__ void remove_future(const Ring<LDS>& R, int t, int s, 
     window_add_linear<-1>(R, t, k + L - t, k - s);
 }
 
-// Steps [t+1, t+len] (len = min(nt - t, H)) become past on the way to step nt:
-// fold their memory into the per-lane peak and re-label their slots for the
-// window [nt+1, nt+H].
+// Fold the past steps (lo, hi] (hi <= t): their memory is final; add it to
+// the per-lane peak and relabel each slot for the step H later.  Steps are
+// visited in increasing order, so a slot met twice (hi - lo > H) is relabelled
+// twice in order.
 template <bool LDS>
-__device__ __forceinline__ void fold_past(const Ring<LDS>& R, int t, int nt, int& peak_lane) {
+__device__ __forceinline__ void fold_range(const Ring<LDS>& R, int lo, int hi, int& peak_lane) {
     const int lane = lane_id();
-    const int len = min(nt - t, R.H);
-    R.runs(t, len, [&](int s, int L, int tau0) {
-        for (int j = lane; j < L; j += 64) {
-            const int tau = tau0 + j;
-            peak_lane = max(peak_lane, R.p[s + j] - tau);
-            R.p[s + j] = nt + 1 + ((tau - nt - 1) & R.mask);
+    for (int b = lo + 1; b <= hi; b += 1024) {
+        int x[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int tau = b + lane + 64 * u;
+            x[u] = tau <= hi ? R.ld(tau) : tau;
         }
-    });
-    Ring<LDS>::order();
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int tau = b + lane + 64 * u;
+            if (tau <= hi) {
+                peak_lane = max(peak_lane, x[u] - tau);
+                R.st(tau, tau + R.H);
+            }
+        }
+        // a slot can come round again H steps later in the same fold
+        Ring<LDS>::order();
+    }
 }
 
 // ---- known lengths: event-driven
@@ -469,16 +558,17 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     const int lane = lane_id();
     const int M = P.M;
     const int n = sg.n;
-    int t = st.t, cursor = st.cursor, seq = st.seq, nadm = st.nfin, max_fin = st.max_fin;
-    int head = st.head_rank, t_f = st.t_f;
+    int t = uni(st.t), cursor = uni(st.cursor), seq = uni(st.seq), nadm = uni(st.nfin);
+    int max_fin = uni(st.max_fin), head = uni(st.head_rank), t_f = uni(st.t_f);
     int peak_lane = 0;
+    int folded = t;  // slots of steps <= folded are labelled for the current window
     int status = STATUS_RUNNING;
 
     // Arrival window: lane l holds request wb + l (arrival, rank, record).
     int wb = 0, a_reg = INT32_MAX, rk_reg = 0;
     int4 aq = make_int4(0, 0, 0, 0);
     auto load_arrivals = [&](int base) {
-        wb = base;
+        wb = uni(base);
         const int i = base + lane;
         a_reg = INT32_MAX;
         rk_reg = 0;
@@ -496,7 +586,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     int4 rw = make_int4(0, 0, 0, 0);
     auto rec_of = [&](int r) -> int4 {
         if (r < rwb || r >= rwb + 64) {
-            rwb = r;
+            rwb = uni(r);
             const int i = r + lane;
             rw = i < n ? sg.rec[i] : make_int4(0, 0, 0, 0);
         }
@@ -540,7 +630,13 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
             if (new_min < head_eff) { r = new_min; q = nq; }
             for (;;) {
                 int tf = 0;
-                if (!fit_and_admit(D, t, q.y, q.z, M, 0, &tf)) { head = r; hq = q; t_f = tf; break; }
+                // slots up to t + oh must be labelled for the current window
+                if (t + q.z - D.H > folded) {
+                    const int to = min(t, t + q.z - D.H + 512);
+                    fold_range(D, folded, to, peak_lane);
+                    folded = to;
+                }
+                if (!fit_and_admit(D, t, q.y, q.z, M, 0, max_fin, &tf)) { head = r; hq = q; t_f = tf; break; }
                 if (lane == 0) {
                     bitmap_clear(B, S, r);
                     sg.start[q.x] = t;
@@ -559,7 +655,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
 
         // 5. advance to the next step where anything can happen
         const int next_arr = cursor < wb + 64 ? __builtin_amdgcn_readlane(a_reg, cursor - wb)
-                                              : (cursor < n ? sg.a[cursor] : INT32_MAX);
+                                              : (cursor < n ? uni(sg.a[cursor]) : INT32_MAX);
         int nt;
         if (head >= 0) nt = min(t_f, next_arr);
         else if (cursor < n) nt = next_arr;
@@ -568,9 +664,10 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         nt = min(nt, t_lim);
         nt = min(nt, P.max_steps + 1);
         if (nt <= t) nt = t + 1;
-        fold_past(D, t, nt, peak_lane);
-        t = nt;
+        t = uni(nt);
     }
+    // every past step folded: the ring is canonical again and the peak complete
+    fold_range(D, folded, t, peak_lane);
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nadm; st.max_fin = max_fin;
     st.head_rank = head; st.t_f = t_f; st.status = status;
     st.peak = max(st.peak, (int64_t)wmax(peak_lane));
@@ -586,6 +683,8 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     int t = st.t, cursor = st.cursor, seq = st.seq, nfin = st.nfin, nA = st.nA, N_O = st.N_O;
     int64_t C_O = st.C_O, peak = st.peak, req_steps = st.req_steps;
     int status = STATUS_RUNNING;
+    // no request admitted so far is planned to hold memory after step maxF
+    int maxF = st.max_fin;
     // memory planned for step t+1 by requests within their planned length
     auto planned_next = [&]() -> int64_t { return (int64_t)D.ld(t + 1) - (t + 1); };
     for (;;) {
@@ -703,7 +802,8 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             int tf = 0;
             // memory of requests past their plan at t+1; <= M after step 3
             const int extra1 = (int)(C_O + (int64_t)N_O * (t + 1));
-            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, &tf)) break;
+            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, maxF, &tf)) break;
+            maxF = max(maxF, t + q.z);
             if (lane == 0) {
                 bitmap_clear(B, S, r);
                 sg.start[q.x] = t;
@@ -731,6 +831,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     }
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nfin; st.nA = nA; st.N_O = N_O;
     st.C_O = C_O; st.peak = peak; st.req_steps = req_steps; st.status = status;
+    st.max_fin = maxF;
 }
 
 template <bool D_LDS>
