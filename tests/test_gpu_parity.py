@@ -319,9 +319,11 @@ def test_full_config5_against_stored_oracle_digests():
     path = os.path.join(GOLDEN, "oracle_digests.json")
     data = json.load(open(path))["cfg5/svf"]
     b = W.config(5)
-    assert b.max_steps == data["max_steps"]
     say("full config 5: 64 x 200000")
     g = gpu_run(b)["svf"]
+    # with known lengths neither run can reach its step budget (the budgets of
+    # the sample and the full batch differ), so the outputs do not depend on it
+    assert (g["stats"]["status"] == 0).all()
     for i_str, ent in data["instances"].items():
         i = int(i_str)
         lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
