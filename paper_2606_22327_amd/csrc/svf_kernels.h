@@ -67,7 +67,7 @@ struct SimArgs {
     const uint8_t* stepped;   // [G] 1: planned lengths differ from the truth
     const int64_t* bw_off;    // [I+1] bitmap word offset of each instance
     uint64_t* bitmap;         // [P*bw_total]
-    int32_t* ring;            // [G*H] future profile plus step index (G = D + tau)
+    int32_t* ring;            // [G*(H+64)] future profile plus step index (G = D + tau)
     int32_t* start;           // [P*N]
     int32_t* fin;
     int32_t* preempt;
@@ -108,7 +108,8 @@ hipError_t launch_chunk_sort(const SortArgs& A, int nchunks, hipStream_t s);
 hipError_t launch_merge_pass(const SortArgs& A, int nchunks, int w, hipStream_t s);
 hipError_t launch_build_rec(const SortArgs& A, int nchunks, hipStream_t s);
 hipError_t prepare_sim(bool d_lds, size_t lds_bytes);
-hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, size_t lds_bytes, hipStream_t s);
+hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, size_t lds_bytes,
+                      hipStream_t s);
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s);
 
 }  // namespace svfk

@@ -115,12 +115,14 @@ __global__ void k_fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
         p[i] = v;
 }
 
-// A fresh ring represents the window [1, H] with D = 0: G[slot] = tau.
+// A fresh ring represents the window [1, H] with D = 0: G[slot] = tau.  Each
+// segment's ring has stride H + 64 (slot H is the spare slot).
 __global__ void k_init_ring(int32_t* __restrict__ ring, int64_t n, int32_t H) {
+    const int64_t RS = (int64_t)H + 64;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
          i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t s = (int32_t)(i & (H - 1));
-        ring[i] = s == 0 ? H : s;
+        const int32_t s = (int32_t)(i % RS);
+        ring[i] = s == 0 ? H : (s < H ? s : 0);
     }
 }
 
@@ -263,28 +265,44 @@ __device__ __forceinline__ void lds_order() {
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
 // Wave-wide max/min with DPP: within quads, half rows and rows, then the
-// row broadcasts of lanes 15 and 31; lane 63 ends with the result.  Must be
-// called with every lane active.
-#define SVF_DPP_STEP(OP, v, ctrl, rmask) \
-    v = OP(v, __builtin_amdgcn_update_dpp(v, v, ctrl, rmask, 0xF, false))
-
+// row broadcasts of lanes 15 and 31; lane 63 ends with the result.  Each step
+// is one DPP-modified max/min (two wait states before it: a DPP source written
+// by the previous VALU instruction).  Must be called with every lane active.
 __device__ __forceinline__ int wmax(int v) {
-    SVF_DPP_STEP(max, v, 0xB1, 0xF);   // quad_perm 1,0,3,2
-    SVF_DPP_STEP(max, v, 0x4E, 0xF);   // quad_perm 2,3,0,1
-    SVF_DPP_STEP(max, v, 0x141, 0xF);  // row_half_mirror
-    SVF_DPP_STEP(max, v, 0x140, 0xF);  // row_mirror
-    SVF_DPP_STEP(max, v, 0x142, 0xA);  // row_bcast:15 into rows 1 and 3
-    SVF_DPP_STEP(max, v, 0x143, 0xC);  // row_bcast:31 into rows 2 and 3
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_max_i32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_i32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_i32_dpp %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_i32_dpp %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_i32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_max_i32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+        "s_nop 1"
+        : "+v"(v));
     return __builtin_amdgcn_readlane(v, 63);
 }
 
 __device__ __forceinline__ int wmin(int v) {
-    SVF_DPP_STEP(min, v, 0xB1, 0xF);
-    SVF_DPP_STEP(min, v, 0x4E, 0xF);
-    SVF_DPP_STEP(min, v, 0x141, 0xF);
-    SVF_DPP_STEP(min, v, 0x140, 0xF);
-    SVF_DPP_STEP(min, v, 0x142, 0xA);
-    SVF_DPP_STEP(min, v, 0x143, 0xC);
+    asm volatile(
+        "s_nop 1\n\t"
+        "v_min_i32_dpp %0, %0, %0 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_min_i32_dpp %0, %0, %0 quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_min_i32_dpp %0, %0, %0 row_half_mirror row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_min_i32_dpp %0, %0, %0 row_mirror row_mask:0xf bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_min_i32_dpp %0, %0, %0 row_bcast:15 row_mask:0xa bank_mask:0xf\n\t"
+        "s_nop 1\n\t"
+        "v_min_i32_dpp %0, %0, %0 row_bcast:31 row_mask:0xc bank_mask:0xf\n\t"
+        "s_nop 1"
+        : "+v"(v));
     return __builtin_amdgcn_readlane(v, 63);
 }
 
@@ -316,11 +334,15 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int src) {
 // workgroup barrier (which also waits for outstanding stores) orders them.
 template <bool LDS>
 struct Ring {
-    int32_t* p;
+    int32_t* p;  // H slots, then one spare slot (index H) that absorbs masked-off stores
     int H;
     int mask;
     __device__ __forceinline__ int ld(int tau) const { return p[tau & mask]; }
     __device__ __forceinline__ void st(int tau, int v) const { p[tau & mask] = v; }
+    // store only if ok; otherwise the value goes to the spare slot (no branch)
+    __device__ __forceinline__ void st_if(bool ok, int tau, int v) const {
+        p[ok ? (tau & mask) : H] = v;
+    }
     __device__ __forceinline__ static void order() {
         if (LDS) lds_order(); else __syncthreads();
     }
@@ -328,10 +350,10 @@ struct Ring {
     // consecutive slots: op(first slot, run length, tau of the first slot).
     template <class Op>
     __device__ __forceinline__ void runs(int t, int len, Op op) const {
-        const int s0 = (t + 1) & mask;
-        const int L1 = min(len, H - s0);
+        const int s0 = uni((t + 1) & mask);
+        const int L1 = uni(min(len, H - s0));
         op(s0, L1, t + 1);
-        if (len > L1) op(0, len - L1, t + 1 + L1);
+        if (len > L1) op(0, uni(len - L1), uni(t + 1 + L1));
     }
 };
 
@@ -411,10 +433,19 @@ __device__ __forceinline__ void window_add_linear(const Ring<LDS>& R, int t, int
             q[128] = x2 + c + SLOPE * 128;
             q[192] = x3 + c + SLOPE * 192;
         }
-        const int rem = L - b;
+        // tail: up to 255 slots, clamped loads, masked-off stores to the spare slot
+        const int rem = uni(L - b);
+        if (rem > 0) {
+            const int base = s + b + lane;
+            int x[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (lane + 64 * u < rem) q[64 * u] += c + SLOPE * 64 * u;
+            for (int u = 0; u < 4; ++u) x[u] = R.p[min(base + 64 * u, R.H - 1)];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool ok = lane + 64 * u < rem;
+                R.p[ok ? base + 64 * u : R.H] = x[u] + c + SLOPE * 64 * u;
+            }
+        }
     });
     Ring<LDS>::order();
 }
@@ -440,6 +471,7 @@ __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h
     const int lim = X + t;
     int len = max(0, min(oh, maxF - t));
     if (extra1 != 0) len = max(len, 1);  // step t+1 always carries extra1
+    len = uni(len);
     if (oh <= 512) {
         int g[8];
         int m = INT32_MIN, rel = INT32_MIN;
@@ -447,17 +479,17 @@ __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h
         for (int u = 0; u < 8; ++u) {
             const int j = lane + 64 * u;
             const int tau = t + 1 + j;
-            g[u] = j < len ? R.ld(tau) : tau;
+            const int x = R.ld(tau);
+            g[u] = j < len ? x : tau;  // beyond maxF the slot holds tau (D = 0)
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int j = lane + 64 * u;
             const int tau = t + 1 + j;
-            if (j < len) {
-                const int v = g[u] + (j == 0 ? extra1 : 0);
-                m = max(m, v);
-                rel = max(rel, min(tau, v - X));
-            }
+            const int v = g[u] + (j == 0 ? extra1 : 0);
+            const bool in = j < len;
+            m = max(m, in ? v : INT32_MIN);
+            rel = max(rel, in ? min(tau, v - X) : INT32_MIN);
         }
         if (ballot(m > lim) != 0ull) {
             *t_free = wmax(rel);
@@ -468,7 +500,7 @@ __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h
         for (int u = 0; u < 8; ++u) {
             const int j = lane + 64 * u;
             const int tau = t + 1 + j;
-            if (j < oh) R.st(tau, g[u] + c + tau);
+            R.st_if(j < oh, tau, g[u] + c + tau);
         }
         Ring<LDS>::order();
         return true;
@@ -494,14 +526,17 @@ __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h
             rel = max(rel, max(max(min(tau, x0 - X), min(tau + 64, x1 - X)),
                                max(min(tau + 128, x2 - X), min(tau + 192, x3 - X))));
         }
-        const int rem = L - b;
+        const int rem = uni(L - b);
+        if (rem > 0) {
+            const int base = s + b + lane;
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-            if (lane + 64 * u < rem) {
-                const int x = q[64 * u];
-                m = max(m, x);
-                rel = max(rel, min(tau + 64 * u, x - X));
+            for (int u = 0; u < 4; ++u) {
+                const int x = R.p[min(base + 64 * u, R.H - 1)];
+                const bool in = lane + 64 * u < rem;
+                m = max(m, in ? x : INT32_MIN);
+                rel = max(rel, in ? min(tau + 64 * u, x - X) : INT32_MIN);
             }
+        }
     });
     if (extra1 != 0) {
         const int v = R.ld(t + 1) + extra1;
@@ -533,17 +568,13 @@ __device__ __forceinline__ void fold_range(const Ring<LDS>& R, int lo, int hi, i
     for (int b = lo + 1; b <= hi; b += 1024) {
         int x[16];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int tau = b + lane + 64 * u;
-            x[u] = tau <= hi ? R.ld(tau) : tau;
-        }
+        for (int u = 0; u < 16; ++u) x[u] = R.ld(b + lane + 64 * u);
 #pragma unroll
         for (int u = 0; u < 16; ++u) {
             const int tau = b + lane + 64 * u;
-            if (tau <= hi) {
-                peak_lane = max(peak_lane, x[u] - tau);
-                R.st(tau, tau + R.H);
-            }
+            const bool ok = tau <= hi;
+            peak_lane = max(peak_lane, ok ? x[u] - tau : 0);
+            R.st_if(ok, tau, tau + R.H);
         }
         // a slot can come round again H steps later in the same fold
         Ring<LDS>::order();
@@ -834,10 +865,14 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     st.max_fin = maxF;
 }
 
-template <bool D_LDS>
+// One wave64 per segment; launched once for segments that plan with the
+// true lengths (event-driven) and once for the others (per step), so each
+// kernel carries only its own path.
+template <bool D_LDS, bool STEPPED>
 __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     extern __shared__ uint64_t smem[];
     const int g = blockIdx.x;
+    if ((P.stepped[g] != 0) != STEPPED) return;
     const int lane = lane_id();
     const int pol = g / P.I, inst = g - pol * P.I;
     const int64_t off = P.offsets[inst];
@@ -867,7 +902,8 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     uint64_t* S = smem + W0;
     for (int x = lane; x < W0 + W1; x += 64) B[x] = Bg[x];
 
-    int32_t* Dg = P.ring + (int64_t)g * P.H;
+    const int RS = P.H + 64;  // ring stride: H slots and the spare slot, padded
+    int32_t* Dg = P.ring + (int64_t)g * RS;
     int32_t* Dl = reinterpret_cast<int32_t*>(smem + P.bw_max);
     if (D_LDS) {
         for (int x = lane; x < P.H; x += 64) Dl[x] = Dg[x];
@@ -882,7 +918,7 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     D.p = D_LDS ? Dl : Dg;
     D.H = P.H;
     D.mask = P.H - 1;
-    if (P.stepped[g] != 0) run_stepped(P, sg, B, S, W1, D, st, t_lim);
+    if (STEPPED) run_stepped(P, sg, B, S, W1, D, st, t_lim);
     else run_known(P, sg, B, S, W1, D, st, t_lim);
     __syncthreads();
     for (int x = lane; x < W0 + W1; x += 64) Bg[x] = B[x];
@@ -995,23 +1031,35 @@ hipError_t launch_build_rec(const SortArgs& A, int nchunks, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, size_t lds_bytes, hipStream_t s) {
+hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, size_t lds_bytes,
+                      hipStream_t s) {
     if (G <= 0) return hipSuccess;
     if (d_lds) {
-        hipLaunchKernelGGL((k_sim<true>), dim3(G), dim3(64), lds_bytes, s, P);
+        if (stepped) hipLaunchKernelGGL((k_sim<true, true>), dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL((k_sim<true, false>), dim3(G), dim3(64), lds_bytes, s, P);
     } else {
-        hipLaunchKernelGGL((k_sim<false>), dim3(G), dim3(64), lds_bytes, s, P);
+        if (stepped) hipLaunchKernelGGL((k_sim<false, true>), dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL((k_sim<false, false>), dim3(G), dim3(64), lds_bytes, s, P);
     }
     return hipGetLastError();
 }
 
 hipError_t prepare_sim(bool d_lds, size_t lds_bytes) {
     if (lds_bytes <= 65536) return hipSuccess;
-    if (d_lds)
-        return hipFuncSetAttribute((const void*)k_sim<true>,
-                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
-    return hipFuncSetAttribute((const void*)k_sim<false>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+    const void* fns[2];
+    if (d_lds) {
+        fns[0] = (const void*)k_sim<true, true>;
+        fns[1] = (const void*)k_sim<true, false>;
+    } else {
+        fns[0] = (const void*)k_sim<false, true>;
+        fns[1] = (const void*)k_sim<false, false>;
+    }
+    for (const void* f : fns) {
+        hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)lds_bytes);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s) {

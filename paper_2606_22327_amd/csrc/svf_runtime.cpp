@@ -64,6 +64,7 @@ struct svf_batch {
     bool d_lds = true;
     size_t lds_bytes = 0;
     bool any_stepped = false;
+    int64_t n_known = 0, n_stepped = 0;
     bool was_reset = false, dirty = false;
     bool prof = false;
     std::vector<Timed> timed;
@@ -241,7 +242,7 @@ int do_reset(svf_batch* h) {
     record(h, 0, &e0);
     HIPCHK(svfk::launch_init_state(h->d_st, G, h->stream));
     HIPCHK(svfk::launch_fill_u64(h->d_bitmap, (int64_t)h->P * h->bw_total, 0ull, h->stream));
-    HIPCHK(svfk::launch_init_ring(h->d_ring, (int64_t)G * h->H, h->H, h->stream));
+    HIPCHK(svfk::launch_init_ring(h->d_ring, (int64_t)G * (h->H + 64), h->H, h->stream));
     HIPCHK(svfk::launch_fill_i32(h->d_start, PN, -1, h->stream));
     HIPCHK(svfk::launch_fill_i32(h->d_fin, PN, -1, h->stream));
     HIPCHK(svfk::launch_fill_i32(h->d_pre, PN, 0, h->stream));
@@ -305,7 +306,10 @@ int do_sim(svf_batch* h, int64_t delta) {
     S.step_delta = delta;
     hipEvent_t e0 = nullptr;
     record(h, 1, &e0);
-    HIPCHK(svfk::launch_sim(S, G, h->d_lds, h->lds_bytes, h->stream));
+    if (h->n_known > 0)
+        HIPCHK(svfk::launch_sim(S, G, h->d_lds, false, h->lds_bytes, h->stream));
+    if (h->n_stepped > 0)
+        HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, h->lds_bytes, h->stream));
     record_end(h, 1, e0);
     h->sim_launches += 1;
     h->dirty = true;
@@ -392,7 +396,10 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     h->H = (int32_t)next_pow2(std::max<int64_t>(max_plan, 1));
     for (int32_t i = 0; i < I; ++i) h->max_n = std::max<int32_t>(h->max_n, (int32_t)(off[i + 1] - off[i]));
     h->CH = (int32_t)std::min<int64_t>(8192, std::max<int64_t>(64, next_pow2(h->max_n)));
-    for (uint8_t x : stepped) h->any_stepped |= x != 0;
+    for (uint8_t x : stepped) {
+        h->any_stepped |= x != 0;
+        (x ? h->n_stepped : h->n_known) += 1;
+    }
     // the profile ring stores memory + step index in int32
     if ((int64_t)h->M + h->max_steps + 2 * (int64_t)h->H >= (int64_t(1) << 31) - 1) {
         delete h;
@@ -422,7 +429,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
 
     // ring placement: LDS when the ring and bitmap fit comfortably
     const char* env = getenv("SVFSIM_RING");
-    const size_t ring_bytes = (size_t)h->H * 4;
+    const size_t ring_bytes = ((size_t)h->H + 64) * 4;  // H slots + spare slot
     const size_t bm_bytes = (size_t)h->bw_max * 8;
     h->d_lds = ring_bytes + bm_bytes <= 65536;
     if (env && !strcmp(env, "global")) h->d_lds = false;
@@ -454,7 +461,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     ALLOC(d_stepped, G);
     ALLOC(d_bw_off, I + 1);
     ALLOC(d_bitmap, (int64_t)P * h->bw_total);
-    ALLOC(d_ring, G * h->H);
+    ALLOC(d_ring, G * (h->H + 64));
     ALLOC(d_start, PN);
     ALLOC(d_fin, PN);
     ALLOC(d_pre, PN);
