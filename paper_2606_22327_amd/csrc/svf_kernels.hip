@@ -450,6 +450,45 @@ __device__ __forceinline__ void window_add_linear(const Ring<LDS>& R, int t, int
     Ring<LDS>::order();
 }
 
+// fit_and_admit for windows of at most 64*U steps: one LDS round trip with U
+// loads per lane in flight, values kept in registers for the update.
+template <int U, bool LDS>
+__device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, int oh, int len,
+                                          int X, int lim, int extra1, int* t_free) {
+    const int lane = lane_id();
+    int g[U];
+    int m = INT32_MIN, rel = INT32_MIN;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int j = lane + 64 * u;
+        const int tau = t + 1 + j;
+        const int x = R.ld(tau);
+        g[u] = j < len ? x : tau;  // beyond maxF the slot holds tau (D = 0)
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int j = lane + 64 * u;
+        const int tau = t + 1 + j;
+        const int v = g[u] + (j == 0 ? extra1 : 0);
+        const bool in = j < len;
+        m = max(m, in ? v : INT32_MIN);
+        rel = max(rel, in ? min(tau, v - X) : INT32_MIN);
+    }
+    if (ballot(m > lim) != 0ull) {
+        *t_free = wmax(rel);
+        return false;
+    }
+    const int c = s_h - t;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int j = lane + 64 * u;
+        const int tau = t + 1 + j;
+        R.st_if(j < oh, tau, g[u] + c + tau);
+    }
+    Ring<LDS>::order();
+    return true;
+}
+
 // Forward-looking check of a candidate (size s_h, planned length oh) started
 // at step t, and its admission when it fits.  extra1 is memory held at t+1
 // only (requests past their planned length).  maxF is a step after which no
@@ -461,8 +500,7 @@ __device__ __forceinline__ void window_add_linear(const Ring<LDS>& R, int t, int
 // violation at tau persists while tau is ahead and the start is earlier than
 // G[tau] - (M - s_h); max_tau min(tau, G[tau] - X) over the window is that
 // step (steps that do not violate contribute at most t).
-// Windows of at most 512 steps take one LDS round trip: eight loads per lane
-// in flight, the values kept in registers for the update.
+// Windows of at most 512 steps take one LDS round trip (fit_small).
 template <bool LDS>
 __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h, int oh, int M,
                                               int extra1, int maxF, int* t_free) {
@@ -472,39 +510,10 @@ __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h
     int len = max(0, min(oh, maxF - t));
     if (extra1 != 0) len = max(len, 1);  // step t+1 always carries extra1
     len = uni(len);
-    if (oh <= 512) {
-        int g[8];
-        int m = INT32_MIN, rel = INT32_MIN;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int j = lane + 64 * u;
-            const int tau = t + 1 + j;
-            const int x = R.ld(tau);
-            g[u] = j < len ? x : tau;  // beyond maxF the slot holds tau (D = 0)
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int j = lane + 64 * u;
-            const int tau = t + 1 + j;
-            const int v = g[u] + (j == 0 ? extra1 : 0);
-            const bool in = j < len;
-            m = max(m, in ? v : INT32_MIN);
-            rel = max(rel, in ? min(tau, v - X) : INT32_MIN);
-        }
-        if (ballot(m > lim) != 0ull) {
-            *t_free = wmax(rel);
-            return false;
-        }
-        const int c = s_h - t;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int j = lane + 64 * u;
-            const int tau = t + 1 + j;
-            R.st_if(j < oh, tau, g[u] + c + tau);
-        }
-        Ring<LDS>::order();
-        return true;
-    }
+    if (oh <= 64) return fit_small<1>(R, t, s_h, oh, len, X, lim, extra1, t_free);
+    if (oh <= 128) return fit_small<2>(R, t, s_h, oh, len, X, lim, extra1, t_free);
+    if (oh <= 256) return fit_small<4>(R, t, s_h, oh, len, X, lim, extra1, t_free);
+    if (oh <= 512) return fit_small<8>(R, t, s_h, oh, len, X, lim, extra1, t_free);
     int m = INT32_MIN, rel = INT32_MIN;
     R.runs(t, len, [&](int s, int L, int tau0) {
         const int32_t* q = R.p + s + lane;
@@ -562,23 +571,29 @@ __device__ __forceinline__ void remove_future(const Ring<LDS>& R, int t, int s, 
 // the per-lane peak and relabel each slot for the step H later.  Steps are
 // visited in increasing order, so a slot met twice (hi - lo > H) is relabelled
 // twice in order.
+template <int U, bool LDS>
+__device__ __forceinline__ void fold_block(const Ring<LDS>& R, int b, int hi, int& peak_lane) {
+    const int lane = lane_id();
+    int x[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = R.ld(b + lane + 64 * u);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int tau = b + lane + 64 * u;
+        const bool ok = tau <= hi;
+        peak_lane = max(peak_lane, ok ? x[u] - tau : 0);
+        R.st_if(ok, tau, tau + R.H);
+    }
+    // a slot can come round again H steps later in the same fold
+    Ring<LDS>::order();
+}
+
 template <bool LDS>
 __device__ __forceinline__ void fold_range(const Ring<LDS>& R, int lo, int hi, int& peak_lane) {
-    const int lane = lane_id();
-    for (int b = lo + 1; b <= hi; b += 1024) {
-        int x[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) x[u] = R.ld(b + lane + 64 * u);
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            const int tau = b + lane + 64 * u;
-            const bool ok = tau <= hi;
-            peak_lane = max(peak_lane, ok ? x[u] - tau : 0);
-            R.st_if(ok, tau, tau + R.H);
-        }
-        // a slot can come round again H steps later in the same fold
-        Ring<LDS>::order();
-    }
+    int b = lo + 1;
+    for (; hi - b >= 1023; b += 1024) fold_block<16>(R, b, hi, peak_lane);
+    for (; hi - b >= 255; b += 256) fold_block<4>(R, b, hi, peak_lane);
+    for (; b <= hi; b += 64) fold_block<1>(R, b, hi, peak_lane);
 }
 
 // ---- known lengths: event-driven
