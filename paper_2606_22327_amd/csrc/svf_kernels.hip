@@ -627,19 +627,32 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     };
     load_arrivals(cursor);
 
-    // Rank window: lane l holds the record of rank rwb + l.
+    // Rank window: lane l holds the record of rank rwb + l (rwb a multiple of
+    // 64, so one window covers one bitmap word).
     int rwb = INT32_MIN / 2;
     int4 rw = make_int4(0, 0, 0, 0);
     auto rec_of = [&](int r) -> int4 {
         if (r < rwb || r >= rwb + 64) {
-            rwb = uni(r);
-            const int i = r + lane;
+            rwb = uni(r & ~63);
+            const int i = rwb + lane;
             rw = i < n ? sg.rec[i] : make_int4(0, 0, 0, 0);
         }
         return readlane4(rw, r - rwb);
     };
     int4 hq = make_int4(0, 0, 0, 0);  // record of the blocked head
     if (head >= 0) hq = rec_of(head);
+
+    // Bitmap word of the current candidate, mirrored in scalar registers for
+    // the admission loop of one step (nothing else writes the bitmap there).
+    int cw = -1;
+    uint64_t cbits = 0ull;
+    auto load_word = [&](int w) {
+        const uint64_t v = B[w];
+        const uint32_t lo = (uint32_t)uni((int)(uint32_t)v);
+        const uint32_t hi = (uint32_t)uni((int)(uint32_t)(v >> 32));
+        cbits = ((uint64_t)hi << 32) | lo;
+        cw = w;
+    };
 
     for (;;) {
         // every request finished by step t-1 (an empty instance is done at t = 0)
@@ -674,6 +687,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
             int r = head;
             int4 q = hq;
             if (new_min < head_eff) { r = new_min; q = nq; }
+            load_word(r >> 6);  // arrivals may have changed any word
             for (;;) {
                 int tf = 0;
                 // slots up to t + oh must be labelled for the current window
@@ -683,8 +697,10 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                     folded = to;
                 }
                 if (!fit_and_admit(D, t, q.y, q.z, M, 0, max_fin, &tf)) { head = r; hq = q; t_f = tf; break; }
+                cbits &= ~(1ull << (r & 63));
                 if (lane == 0) {
-                    bitmap_clear(B, S, r);
+                    B[cw] = cbits;
+                    if (cbits == 0ull) S[cw >> 6] &= ~(1ull << (cw & 63));
                     sg.start[q.x] = t;
                     sg.admit_seq[q.x] = seq;
                     sg.fin[q.x] = t + q.w;
@@ -693,8 +709,13 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                 ++seq;
                 ++nadm;
                 max_fin = max(max_fin, t + q.w);
-                r = bitmap_first(B, S, W1);
-                if (r < 0) { head = -1; break; }
+                if (cbits != 0ull) {
+                    r = cw * 64 + __builtin_ctzll(cbits);
+                } else {
+                    r = bitmap_first(B, S, W1);
+                    if (r < 0) { head = -1; break; }
+                    load_word(r >> 6);
+                }
                 q = rec_of(r);
             }
         }
