@@ -21,6 +21,14 @@ import numpy as np
 from . import build as _build
 
 POLICY_IDS = {"fcfs": 0, "sjf": 1, "svf": 2, "svf1bit": 3}
+RULE_CURRENT = 0x100  # "+cur" suffix: current-capacity admission
+
+
+def policy_code(policy: str) -> int:
+    """'svf' -> 2; 'svf+cur' -> 2 | RULE_CURRENT."""
+    if policy.endswith("+cur"):
+        return POLICY_IDS[policy[:-4]] | RULE_CURRENT
+    return POLICY_IDS[policy]
 STAT_FIELDS = ("makespan", "status", "sum_latency", "request_steps", "peak_mem",
                "preemptions", "t_end", "n_finished")
 
@@ -73,7 +81,7 @@ def run(batch, policy: str, threads: int = 0, t_stop: int = 2 ** 62, max_steps=N
     o = np.ascontiguousarray(batch.output, dtype=np.int32)
     plan = None if batch.plan_len is None else np.ascontiguousarray(batch.plan_len, dtype=np.int32)
     bit = None if batch.long_bit is None else np.ascontiguousarray(batch.long_bit, dtype=np.int8)
-    if policy == "svf1bit" and bit is None:
+    if policy.startswith("svf1bit") and bit is None:
         raise ValueError("svf1bit needs long_bit")
     start = np.empty(max(N, 1), dtype=np.int32)
     finish = np.empty(max(N, 1), dtype=np.int32)
@@ -84,7 +92,7 @@ def run(batch, policy: str, threads: int = 0, t_stop: int = 2 ** 62, max_steps=N
         threads = os.cpu_count() or 1
     ms = batch.max_steps if max_steps is None else max_steps
     lib.oracle_run(I, _ptr(off), _ptr(a), _ptr(s), _ptr(o), _ptr(plan), _ptr(bit),
-                   int(batch.M), POLICY_IDS[policy], int(batch.O0), int(batch.O1),
+                   int(batch.M), policy_code(policy), int(batch.O0), int(batch.O1),
                    int(ms), int(t_stop), int(threads), _ptr(start), _ptr(finish),
                    _ptr(pre), _ptr(seq), _ptr(stats))
     return {"start": start[:N], "finish": finish[:N], "preempt": pre[:N],

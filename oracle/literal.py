@@ -15,7 +15,9 @@ the design notes):
   2. completions t - k_i = o_i leave A;
   3. while the true memory at t+1 exceeds M: evict the largest believed
      remaining volume (latest arrival on ties), eligible again at t+1;
-  4. strict head-of-line admission with the forward-looking check;
+  4. strict head-of-line admission with the forward-looking check (or, for a
+     policy name ending in "+cur", the current-capacity rule of Alg. 1 read
+     literally: the next step's memory including the candidate stays <= M);
   5. request_steps += |A|; peak = max(peak, memory at t+1); t += 1.
 """
 
@@ -41,6 +43,8 @@ def key_of(policy: str, a: int, s: int, ohat: int) -> int:
 def simulate(arrival, prompt, output, M: int, policy: str, plan=None, long_bit=None,
              O0: int = 0, O1: int = 0, max_steps: int = 10 ** 9,
              t_stop: int = 10 ** 18) -> Dict:
+    current_rule = policy.endswith("+cur")
+    policy = policy[:-4] if current_rule else policy
     n = len(arrival)
     a = [int(x) for x in arrival]
     s = [int(x) for x in prompt]
@@ -112,8 +116,11 @@ def simulate(arrival, prompt, output, M: int, policy: str, plan=None, long_bit=N
             h = min(W, key=lambda i: key[i])
             k[h] = t          # tentatively started at t
             members = A | {h}
-            horizon = max(planned_finish(i, t) for i in members)
-            ok = all(mem_at(tau, members, t) <= M for tau in range(t + 1, horizon + 1))
+            if current_rule:
+                ok = sum(s[i] + t + 1 - k[i] for i in members) <= M
+            else:
+                horizon = max(planned_finish(i, t) for i in members)
+                ok = all(mem_at(tau, members, t) <= M for tau in range(t + 1, horizon + 1))
             if not ok:
                 k[h] = None
                 break

@@ -33,6 +33,13 @@
  *                   otherwise stop (strict head of line, no backfilling);
  *   5. advance:     request_steps += |A|, peak = max(peak, memory at t+1).
  *
+ * Admission rule.  The default is the forward-looking check above.  The
+ * alternative "current capacity" rule reads Alg. 1's Process 2 literally (pop
+ * the head while the KV cache has room): h is admitted iff the memory of the
+ * next step, sum_{i in A} (s_i + t+1 - k_i) + (s_h + 1), stays <= M; later
+ * growth beyond M is then resolved by step 3's eviction.  A policy code selects
+ * it by adding RULE_CURRENT (0x100) to the policy number.
+ *
  * Priority keys (lower first; ties by arrival then index):
  *   FCFS      a_i
  *   SJF       o^_i
@@ -60,6 +67,7 @@
 #define POL_SJF 1
 #define POL_SVF 2
 #define POL_SVF1BIT 3
+#define RULE_CURRENT 0x100
 
 #define NSTATS 8
 /* stats layout per instance: makespan, status, sum_latency, request_steps,
@@ -70,7 +78,7 @@ typedef struct {
     const int32_t *a, *s, *o, *plan; /* plan may be NULL */
     const int8_t *bit;               /* may be NULL */
     int64_t M;
-    int32_t policy, O0, O1;
+    int32_t policy, rule, O0, O1;
     int64_t max_steps, t_stop;
     int32_t *start, *finish, *preempt, *admit_seq;
     int64_t *stats;
@@ -185,6 +193,21 @@ static void simulate(inst_job *J) {
             int32_t h = W[hx];
             int64_t Fh = t + ohat[h];
             int feasible = 1;
+            if (J->rule == RULE_CURRENT) {
+                /* memory of the next step only */
+                int64_t mem_next = s[h] + 1;
+                for (int32_t x = 0; x < nA; ++x) {
+                    int32_t j = A[x];
+                    mem_next += s[j] + (t + 1) - k[j];
+                }
+                if (mem_next > M) break;
+                k[h] = t;
+                J->start[h] = (int32_t)t;
+                J->admit_seq[h] = (int32_t)seq++;
+                A[nA++] = h;
+                W[hx] = W[--nW];
+                continue;
+            }
             /* checkpoints: every planned finish of an active request up to F_h,
              * and F_h itself */
             for (int32_t c = -1; c < nA && feasible; ++c) {
@@ -264,7 +287,8 @@ static void *worker(void *p) {
 }
 
 /*
- * Simulate every instance of a batch under one policy.
+ * Simulate every instance of a batch under one policy (policy number, plus
+ * RULE_CURRENT for the current-capacity admission rule).
  *   offsets[num_instances+1]: CSR offsets into the per-request arrays
  *   plan, bit: may be NULL (plan NULL => believed length = true length)
  *   t_stop: stop before processing step t_stop (status 2), or a huge value
@@ -285,7 +309,8 @@ int oracle_run(int32_t num_instances, const int64_t *offsets, const int32_t *a,
         J->a = a + lo; J->s = s + lo; J->o = o + lo;
         J->plan = plan ? plan + lo : NULL;
         J->bit = bit ? bit + lo : NULL;
-        J->M = M; J->policy = policy; J->O0 = O0; J->O1 = O1;
+        J->M = M; J->policy = policy & 0xFF; J->rule = policy & RULE_CURRENT;
+        J->O0 = O0; J->O1 = O1;
         J->max_steps = max_steps; J->t_stop = t_stop;
         J->start = start + lo; J->finish = finish + lo;
         J->preempt = preempt + lo; J->admit_seq = admit_seq + lo;

@@ -17,6 +17,9 @@ Given one instance (a, s, o, believed lengths o^, policy) and a schedule
   V5  every admission passed the forward-looking check against the requests
       running at that moment (with the lengths the scheduler believed)
 
+With rule="current" (Alg. 1's Process 2 read literally) V4 and V5 use the
+memory of the next step only, including the candidate's first token.
+
 With V1-V5 the admissions at every step are the longest feasible prefix of the
 waiting requests in priority order, so by induction over t they fix the whole
 schedule: a simulator that passes the validator on an instance has produced
@@ -92,8 +95,13 @@ def _planned_ok(t, cand_s, cand_oh, members, s, oh, k, M):
     return bool((mem <= M).all())
 
 
+def _current_ok(t, cand_s, members, s, k, M):
+    """Next-step memory of the running requests plus the candidate's s + 1."""
+    return int((s[members] + t + 1 - k[members]).sum()) + cand_s + 1 <= M
+
+
 def validate(a, s, o, start, admit_seq, M: int, policy: str, ohat=None,
-             finish=None) -> Dict:
+             finish=None, rule: str = "lookahead") -> Dict:
     """Raise AssertionError on the first violated condition; return the
     statistics recomputed from the schedule."""
     a = np.asarray(a, dtype=np.int64)
@@ -123,9 +131,7 @@ def validate(a, s, o, start, admit_seq, M: int, policy: str, ohat=None,
     rank = np.empty(n, dtype=np.int64)
     rank[order] = np.arange(n)
     # V3-V5, step by step over every step where something waits or starts
-    events = np.unique(np.concatenate([a, k]))
     t_last = int(k.max())
-    started_by = {}
     for t in range(0, t_last + 1):
         waiting = np.nonzero((a <= t) & (k >= t))[0]
         if waiting.size == 0:
@@ -139,14 +145,18 @@ def validate(a, s, o, start, admit_seq, M: int, policy: str, ohat=None,
         running = np.nonzero((k < t) & (fin > t))[0]
         members = running
         # V5: each admission fitted against what ran at that moment
+        def fits(j, members):
+            if rule == "current":
+                return _current_ok(t, s[j], members, s, k, M)
+            return _planned_ok(t, s[j], oh[j], members, s, oh, k, M)
         for j in adm_sorted.tolist():
-            assert _planned_ok(t, s[j], oh[j], members, s, oh, k, M), \
+            assert fits(j, members), \
                 f"V5: step {t}: request {j} was admitted although it did not fit"
             members = np.append(members, j)
         # V4: the next request in line did not fit
         if adm.size < waiting.size:
             h = int(w_sorted[adm.size])
-            assert not _planned_ok(t, s[h], oh[h], members, s, oh, k, M), \
+            assert not fits(h, members), \
                 f"V4: step {t}: request {h} fitted but was not admitted"
     return {"makespan": int(fin.max()), "sum_latency": int((fin - a).sum()),
             "request_steps": int(o.sum()), "peak_mem": int(prof.max())}

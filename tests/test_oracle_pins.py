@@ -301,7 +301,7 @@ def test_c_oracle_matches_literal(seed):
     for kw in (dict(), dict(bits=True), dict(plan_noise=True)):
         b = W.random_small(seed, instances=10, n_max=13, s_max=6, o_max=10, M=24,
                            gap_mean=0.8 if seed % 2 else 0.0, **kw)
-        for pol in b.policies:
+        for pol in b.policies + tuple(p + "+cur" for p in b.policies):
             r = oracle.run(b, pol, threads=2)
             for i in range(b.num_instances):
                 lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
@@ -356,3 +356,51 @@ def test_step_budget_and_partial_runs():
             L = literal.simulate(d["arrival"], d["prompt"], d["output"], b.M, pol, max_steps=ms)
             assert int(cut["stats"][i, 1]) == L["status"]
             assert int(cut["stats"][i, 3]) == L["request_steps"]
+
+
+# ------------------------------------ current-capacity admission (NEXT f1)
+
+def test_current_capacity_rule_validator_and_invariants():
+    """Alg. 1's Process 2 read literally: admit while the next step's memory
+    (running requests plus the candidate's first token) fits.  Runs without
+    preemption are pinned by the validator with that rule; every run keeps the
+    true memory <= M at every step (eviction) and finish = start + o."""
+    checked = 0
+    for seed in range(4):
+        b = W.random_small(20 + seed, instances=12, n_max=30, s_max=8, o_max=12, M=40,
+                           gap_mean=0.7)
+        for pol in ("svf+cur", "sjf+cur", "fcfs+cur"):
+            r = oracle.run(b, pol)
+            assert (r["stats"][:, 1] == 0).all()
+            for i in range(b.num_instances):
+                lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+                d = b.instance(i)
+                k = r["start"][lo:hi]
+                assert (r["finish"][lo:hi] == k + d["output"]).all()
+                prof = validate.true_profile(d["prompt"], d["output"], k,
+                                             int(r["finish"][lo:hi].max()) + 1 if hi > lo else 1)
+                assert int(prof.max()) <= b.M
+                if (r["preempt"][lo:hi] == 0).all():
+                    validate.validate(d["arrival"], d["prompt"], d["output"], k,
+                                      r["admit_seq"][lo:hi], b.M, pol[:-4], rule="current",
+                                      finish=r["finish"][lo:hi])
+                    checked += 1
+    assert checked > 20
+
+
+def test_current_capacity_equals_lookahead_with_ample_memory():
+    b = W.config(2, instances=3, n=200)
+    big = W.assemble("big", [b.instance(i) for i in range(3)],
+                     int((b.prompt.astype(np.int64) + b.output).sum()), ("svf",))
+    r1 = oracle.run(big, "svf")
+    r2 = oracle.run(big, "svf+cur")
+    for f in ("start", "finish", "admit_seq"):
+        assert np.array_equal(r1[f], r2[f])
+
+
+def test_current_capacity_preempts_where_lookahead_does_not():
+    b = W.config(4, instances=2, n=600)
+    la = oracle.run(b, "svf")
+    cur = oracle.run(b, "svf+cur")
+    assert int(la["stats"][:, 5].sum()) == 0
+    assert int(cur["stats"][:, 5].sum()) > 0
