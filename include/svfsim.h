@@ -48,6 +48,17 @@ enum {
     SVF_POLICY_SVF1BIT = 3  /* the same with o^_i = b_i ? O1 : O0  (Eq. 2)   */
 };
 
+/* Admission rule, added to a policy number (e.g. SVF_POLICY_SVF |
+ * SVF_ADMIT_CURRENT).  The default is the forward-looking check (no future
+ * step over M, Appendix E.2).  SVF_ADMIT_CURRENT reads Alg. 1's Process 2
+ * literally: the head is admitted while the memory of the next step, with the
+ * head's first token, fits; growth beyond M later is resolved by evicting the
+ * running request with the largest believed remaining volume. */
+enum {
+    SVF_ADMIT_LOOKAHEAD = 0,
+    SVF_ADMIT_CURRENT = 0x100
+};
+
 /* Return codes. */
 enum {
     SVF_OK = 0,
@@ -85,7 +96,8 @@ typedef struct svf_batch svf_batch; /* opaque handle */
  *                                                               int8 [N] or NULL
  *   M                KV budget in tokens, 1 <= M < 2^30
  *   num_policies     1..8 policies run side by side on the same instances
- *   policies         host array [num_policies] of SVF_POLICY_*
+ *   policies         host array [num_policies] of SVF_POLICY_*, each optionally
+ *                    plus SVF_ADMIT_CURRENT
  *   O0, O1           1-bit proxy lengths (>= 1 when SVF1BIT is listed)
  *   max_steps        stop an instance after step max_steps (0 <= max_steps
  *                    < 2^30); such instances report SVF_STATUS_EXHAUSTED
@@ -95,6 +107,9 @@ typedef struct svf_batch svf_batch; /* opaque handle */
  *                    during svf_create (copied into the handle's own buffers)
  *
  * The packed priority key (key << 32 | index) must fit: every key < 2^32.
+ * Memory totals are kept in 32 bits: M + max_steps + 2 * (longest planned
+ * length rounded up to a power of two) < 2^31, where under SVF_ADMIT_CURRENT
+ * an instance's sum of s_i + o^_i takes M's place when larger.
  */
 typedef struct svf_batch_desc {
     int32_t num_instances;

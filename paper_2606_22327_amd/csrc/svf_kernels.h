@@ -8,6 +8,7 @@
 namespace svfk {
 
 enum { POLICY_FCFS = 0, POLICY_SJF = 1, POLICY_SVF = 2, POLICY_SVF1BIT = 3 };
+enum { ADMIT_CURRENT = 0x100 };  // added to a policy code: next-step admission
 enum { STATUS_DONE = 0, STATUS_EXHAUSTED = 1, STATUS_RUNNING = 2 };
 
 // Per-segment (instance x policy) simulation state, kept in HBM between launches.
@@ -64,7 +65,8 @@ struct SimArgs {
     const int32_t* a;
     const int4* rec;
     const int32_t* rank;
-    const uint8_t* stepped;   // [G] 1: planned lengths differ from the truth
+    const uint8_t* stepped;   // [G] 1: per-step path (plans differ or next-step admission)
+    const int32_t* policies;  // [P] policy codes
     const int64_t* bw_off;    // [I+1] bitmap word offset of each instance
     uint64_t* bitmap;         // [P*bw_total]
     int32_t* ring;            // [G*(H+64)] future profile plus step index (G = D + tau)

@@ -148,7 +148,7 @@ __global__ __launch_bounds__(NT) void k_chunk_sort(SortArgs A) {
     const int64_t off = A.offsets[inst];
     const int n = (int)(A.offsets[inst + 1] - off);
     const int len = min(CH, n - lo);
-    const int policy = A.policies[pol];
+    const int policy = A.policies[pol] & 0xFF;
     for (int j = threadIdx.x; j < CH; j += NT) {
         uint64_t v = ~0ull;
         if (j < len) {
@@ -218,7 +218,7 @@ __global__ __launch_bounds__(256) void k_build_rec(SortArgs A) {
     const int64_t off = A.offsets[inst];
     const int n = (int)(A.offsets[inst + 1] - off);
     const int len = min(A.CH, n - lo);
-    const int policy = A.policies[pol];
+    const int policy = A.policies[pol] & 0xFF;
     const uint64_t* keys = A.keys_in + (int64_t)pol * A.N + off;
     int4* rec = A.rec + (int64_t)pol * A.N + off;
     int32_t* rank = A.rank + (int64_t)pol * A.N + off;
@@ -454,7 +454,7 @@ __device__ __forceinline__ void window_add_linear(const Ring<LDS>& R, int t, int
 // loads per lane in flight, values kept in registers for the update.
 template <int U, bool LDS>
 __device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, int oh, int len,
-                                          int X, int lim, int extra1, int* t_free) {
+                                          int live, int X, int lim, int extra1, int* t_free) {
     const int lane = lane_id();
     int g[U];
     int m = INT32_MIN, rel = INT32_MIN;
@@ -463,7 +463,7 @@ __device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, in
         const int j = lane + 64 * u;
         const int tau = t + 1 + j;
         const int x = R.ld(tau);
-        g[u] = j < len ? x : tau;  // beyond maxF the slot holds tau (D = 0)
+        g[u] = j < live ? x : tau;  // beyond maxF the slot holds tau (D = 0)
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -490,7 +490,8 @@ __device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, in
 }
 
 // Forward-looking check of a candidate (size s_h, planned length oh) started
-// at step t, and its admission when it fits.  extra1 is memory held at t+1
+// at step t, and its admission when it fits; chk = 1 checks the next step
+// only (current-capacity admission).  extra1 is memory held at t+1
 // only (requests past their planned length).  maxF is a step after which no
 // running request is planned to hold memory (D = 0 there, so the candidate
 // alone, s_h + oh <= M, always fits); the check stops there.  If the
@@ -503,17 +504,20 @@ __device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, in
 // Windows of at most 512 steps take one LDS round trip (fit_small).
 template <bool LDS>
 __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h, int oh, int M,
-                                              int extra1, int maxF, int* t_free) {
+                                              int extra1, int maxF, int* t_free, int chk = 1 << 30) {
     const int lane = lane_id();
     const int X = M - s_h;
     const int lim = X + t;
-    int len = max(0, min(oh, maxF - t));
+    // steps of the candidate's window that hold planned memory, and the part checked
+    const int live = uni(max(0, min(oh, maxF - t)));
+    int len = min(live, chk);
     if (extra1 != 0) len = max(len, 1);  // step t+1 always carries extra1
     len = uni(len);
-    if (oh <= 64) return fit_small<1>(R, t, s_h, oh, len, X, lim, extra1, t_free);
-    if (oh <= 128) return fit_small<2>(R, t, s_h, oh, len, X, lim, extra1, t_free);
-    if (oh <= 256) return fit_small<4>(R, t, s_h, oh, len, X, lim, extra1, t_free);
-    if (oh <= 512) return fit_small<8>(R, t, s_h, oh, len, X, lim, extra1, t_free);
+    const int ld = max(len, live);
+    if (oh <= 64) return fit_small<1>(R, t, s_h, oh, len, ld, X, lim, extra1, t_free);
+    if (oh <= 128) return fit_small<2>(R, t, s_h, oh, len, ld, X, lim, extra1, t_free);
+    if (oh <= 256) return fit_small<4>(R, t, s_h, oh, len, ld, X, lim, extra1, t_free);
+    if (oh <= 512) return fit_small<8>(R, t, s_h, oh, len, ld, X, lim, extra1, t_free);
     int m = INT32_MIN, rel = INT32_MIN;
     R.runs(t, len, [&](int s, int L, int tau0) {
         const int32_t* q = R.p + s + lane;
@@ -752,6 +756,9 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     int status = STATUS_RUNNING;
     // no request admitted so far is planned to hold memory after step maxF
     int maxF = st.max_fin;
+    // current-capacity admission checks the next step only
+    const int pol = blockIdx.x / P.I;
+    const int chk = (P.policies[pol] & ADMIT_CURRENT) ? 1 : (1 << 30);
     // memory planned for step t+1 by requests within their planned length
     auto planned_next = [&]() -> int64_t { return (int64_t)D.ld(t + 1) - (t + 1); };
     for (;;) {
@@ -869,7 +876,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             int tf = 0;
             // memory of requests past their plan at t+1; <= M after step 3
             const int extra1 = (int)(C_O + (int64_t)N_O * (t + 1));
-            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, maxF, &tf)) break;
+            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, maxF, &tf, chk)) break;
             maxF = max(maxF, t + q.z);
             if (lane == 0) {
                 bitmap_clear(B, S, r);

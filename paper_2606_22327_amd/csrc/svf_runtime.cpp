@@ -142,18 +142,24 @@ struct HostView {
 
 // Everything that can be checked without a GPU.
 int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64_t>& off,
-             int64_t N, std::vector<uint8_t>* stepped, int64_t* max_plan) {
+             int64_t N, std::vector<uint8_t>* stepped, int64_t* max_plan, int64_t* max_profile) {
     const int32_t I = d->num_instances, P = d->num_policies;
     bool has1bit = false;
-    for (int p = 0; p < P; ++p) has1bit |= d->policies[p] == SVF_POLICY_SVF1BIT;
+    for (int p = 0; p < P; ++p) has1bit |= (d->policies[p] & 0xFF) == SVF_POLICY_SVF1BIT;
     if (N > 0 && (!v.a || !v.s || !v.o))
         return fail(SVF_EINVAL, "arrival, prompt and output must not be NULL");
     if (has1bit && N > 0 && !v.bit) return fail(SVF_EINVAL, "SVF1BIT needs long_bit");
     if (has1bit && (d->O0 < 1 || d->O1 < 1)) return fail(SVF_EINVAL, "SVF1BIT needs O0, O1 >= 1");
     *max_plan = 1;
+    // Largest planned memory total at one future step.  The forward-looking
+    // check keeps it <= M; with next-step admission only, the requests of an
+    // instance bound it together: sum of s + o^.
+    *max_profile = d->M;
     stepped->assign((size_t)P * I, 0);
+    std::vector<int64_t> cur_total(P);
     for (int32_t i = 0; i < I; ++i) {
         const int64_t lo = off[i], hi = off[i + 1];
+        std::fill(cur_total.begin(), cur_total.end(), 0);
         for (int64_t j = lo; j < hi; ++j) {
             const int32_t a = v.a[j], s = v.s[j], o = v.o[j];
             if (a < 0 || a >= kLimit30)
@@ -169,7 +175,8 @@ int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64
             if (v.bit && v.bit[j] != 0 && v.bit[j] != 1)
                 return fail(SVF_EINVAL, "instance %d request %lld: long_bit %d not 0/1", i, (long long)(j - lo), v.bit[j]);
             for (int p = 0; p < P; ++p) {
-                const int pol = d->policies[p];
+                const int pol = d->policies[p] & 0xFF;
+                const bool current_rule = (d->policies[p] & SVF_ADMIT_CURRENT) != 0;
                 int64_t oh;
                 if (pol == SVF_POLICY_SVF1BIT) oh = v.bit[j] ? d->O1 : d->O0;
                 else oh = v.plan ? v.plan[j] : o;
@@ -185,10 +192,14 @@ int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64
                 if (key >= (uint64_t(1) << 32))
                     return fail(SVF_EINVAL, "instance %d request %lld: priority key %llu >= 2^32", i,
                                 (long long)(j - lo), (unsigned long long)key);
-                if (oh != o) (*stepped)[(size_t)p * I + i] = 1;
+                // eviction is only possible when plans differ from the truth
+                // or when admission looks at the next step only
+                if (oh != o || current_rule) (*stepped)[(size_t)p * I + i] = 1;
                 *max_plan = std::max(*max_plan, oh);
+                if (current_rule) cur_total[p] += s + oh;
             }
         }
+        for (int p = 0; p < P; ++p) *max_profile = std::max(*max_profile, cur_total[p]);
     }
     return SVF_OK;
 }
@@ -200,9 +211,12 @@ int check_desc_shape(const svf_batch_desc* d, std::vector<int64_t>* off, int64_t
     if (d->num_policies < 1 || d->num_policies > 8)
         return fail(SVF_EINVAL, "num_policies must be in 1..8 (got %d)", d->num_policies);
     if (!d->policies) return fail(SVF_EINVAL, "policies is NULL");
-    for (int p = 0; p < d->num_policies; ++p)
-        if (d->policies[p] < SVF_POLICY_FCFS || d->policies[p] > SVF_POLICY_SVF1BIT)
+    for (int p = 0; p < d->num_policies; ++p) {
+        const int base = d->policies[p] & 0xFF, rule = d->policies[p] & ~0xFF;
+        if (base < SVF_POLICY_FCFS || base > SVF_POLICY_SVF1BIT ||
+            (rule != SVF_ADMIT_LOOKAHEAD && rule != SVF_ADMIT_CURRENT))
             return fail(SVF_EINVAL, "unknown policy %d", d->policies[p]);
+    }
     if (d->M < 1 || d->M >= kLimit30) return fail(SVF_EINVAL, "M must be in [1, 2^30)");
     if (d->max_steps < 0 || d->max_steps >= kLimit30)
         return fail(SVF_EINVAL, "max_steps must be in [0, 2^30)");
@@ -287,6 +301,7 @@ int do_sim(svf_batch* h, int64_t delta) {
     S.rec = h->d_rec;
     S.rank = h->d_rank;
     S.stepped = h->d_stepped;
+    S.policies = h->d_pol;
     S.bw_off = h->d_bw_off;
     S.bitmap = h->d_bitmap;
     S.ring = h->d_ring;
@@ -380,8 +395,8 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
         }
     }
     std::vector<uint8_t> stepped;
-    int64_t max_plan = 1;
-    RETCHK(validate(d, v, off, N, &stepped, &max_plan));
+    int64_t max_plan = 1, max_profile = 0;
+    RETCHK(validate(d, v, off, N, &stepped, &max_plan, &max_profile));
 
     svf_batch* h = new (std::nothrow) svf_batch();
     if (!h) return fail(SVF_ENOMEM, "host allocation failed");
@@ -401,10 +416,11 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
         (x ? h->n_stepped : h->n_known) += 1;
     }
     // the profile ring stores memory + step index in int32
-    if ((int64_t)h->M + h->max_steps + 2 * (int64_t)h->H >= (int64_t(1) << 31) - 1) {
+    if (max_profile + h->max_steps + 2 * (int64_t)h->H >= (int64_t(1) << 31) - 1) {
         delete h;
-        return fail(SVF_EINVAL, "M + max_steps + 2 * (longest planned length, rounded up to a power "
-                                "of two) must stay below 2^31");
+        return fail(SVF_EINVAL, "M (or, under SVF_ADMIT_CURRENT, an instance's sum of s + planned "
+                                "length) + max_steps + 2 * (longest planned length, rounded up to "
+                                "a power of two) must stay below 2^31");
     }
 
     // chunk table (segment, first position) and bitmap offsets

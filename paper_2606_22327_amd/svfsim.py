@@ -22,6 +22,14 @@ LIB_PATH = os.path.join(_PKG, "libsvfsim.so")
 
 POLICY = {"fcfs": 0, "sjf": 1, "svf": 2, "svf1bit": 3}
 POLICY_NAMES = {v: k for k, v in POLICY.items()}
+ADMIT_CURRENT = 0x100  # policy name suffix "+cur": current-capacity admission
+
+
+def policy_code(name: str) -> int:
+    """'svf' -> SVF_POLICY_SVF; 'svf+cur' -> SVF_POLICY_SVF | SVF_ADMIT_CURRENT."""
+    if name.endswith("+cur"):
+        return POLICY[name[:-4]] | ADMIT_CURRENT
+    return POLICY[name]
 ERRORS = {0: "SVF_OK", -1: "SVF_EINVAL", -2: "SVF_ENOMEM", -3: "SVF_EHIP",
           -4: "SVF_EINFEASIBLE", -5: "SVF_ESTATE"}
 STATUS = {0: "done", 1: "exhausted", 2: "running"}
@@ -141,7 +149,7 @@ class Simulator:
         on_dev = _is_torch(arrival)
         self._keep = []
         off = np.ascontiguousarray(offsets, dtype=np.int64)
-        pol = np.ascontiguousarray([POLICY[p] for p in self.policies], dtype=np.int32)
+        pol = np.ascontiguousarray([policy_code(p) for p in self.policies], dtype=np.int32)
         self._keep += [off, pol]
         d = BatchDesc()
         d.num_instances = len(off) - 1

@@ -75,7 +75,13 @@ class Batch:
         parts = [self.instance(int(i)) for i in ids]
         return assemble(self.name + "[sub]", parts, self.M, self.policies,
                         O0=self.O0, O1=self.O1, max_steps=self.max_steps,
-                        meta=dict(self.meta, subset=list(map(int, ids))))
+                        meta=self._subset_meta(ids))
+
+    def _subset_meta(self, ids: Sequence[int]) -> Dict:
+        meta = dict(self.meta, subset=list(map(int, ids)))
+        if "instance_ids" in meta:
+            meta["instance_ids"] = np.asarray(meta["instance_ids"])[np.asarray(ids, dtype=np.int64)]
+        return meta
 
 
 def _rng(cfg: int, inst: int) -> np.random.Generator:
@@ -135,8 +141,9 @@ def default_max_steps(b: Batch) -> int:
 
     With plan == true length, every step either advances an active request or
     waits for an arrival, so the last finish is at most max(a) + sum(o).  When
-    the scheduler plans with other lengths (1-bit policy, predictor noise),
-    preemption can waste steps, so the budget is widened 64 times.
+    the scheduler plans with other lengths (1-bit policy, predictor noise), or
+    admits on the next step's memory only, preemption can waste steps, so the
+    budget is widened 64 times.
     """
     worst = 1
     for i in range(b.num_instances):
@@ -145,7 +152,8 @@ def default_max_steps(b: Batch) -> int:
             w = int(b.arrival[lo:hi].max()) + int(b.output[lo:hi].astype(np.int64).sum())
             worst = max(worst, w)
     worst += 1
-    planned_differently = ("svf1bit" in b.policies) or (b.plan_len is not None)
+    planned_differently = any(p.startswith("svf1bit") or p.endswith("+cur")
+                              for p in b.policies) or (b.plan_len is not None)
     return worst * 64 if planned_differently else worst
 
 
@@ -210,13 +218,15 @@ def gen_instance(cfg: int, inst: int, n: Optional[int] = None,
     raise ValueError(f"unknown configuration {cfg}")
 
 
+# o_cap: the generation cap of each workload (largest output length it draws);
+# a length predictor answers inside it.
 CONFIGS = {
-    1: dict(instances=256, M=512, policies=("svf", "sjf", "fcfs")),
-    2: dict(instances=4096, M=65536, policies=("svf", "sjf", "fcfs")),
+    1: dict(instances=256, M=512, policies=("svf", "sjf", "fcfs"), o_cap=64),
+    2: dict(instances=4096, M=65536, policies=("svf", "sjf", "fcfs"), o_cap=2048),
     3: dict(instances=4096, M=65536, policies=("svf1bit", "svf", "sjf", "fcfs"),
-            O0=16, O1=724),
-    4: dict(instances=16384, M=262144, policies=("svf",)),
-    5: dict(instances=64, M=2 ** 21, policies=("svf",)),
+            O0=16, O1=724, o_cap=2048),
+    4: dict(instances=16384, M=262144, policies=("svf",), o_cap=4096),
+    5: dict(instances=64, M=2 ** 21, policies=("svf",), o_cap=8192),
 }
 
 CONFIG_TITLES = {
@@ -249,8 +259,35 @@ def config(cfg: int, instances=None, n: Optional[int] = None,
     b = assemble(f"cfg{cfg}", parts, spec["M"], tuple(policies or spec["policies"]),
                  O0=spec.get("O0", 0), O1=spec.get("O1", 0),
                  meta={"cfg": cfg, "ids": list(map(int, ids)) if not isinstance(ids, range)
-                       else [ids.start, ids.stop], "n": n})
+                       else [ids.start, ids.stop], "n": n,
+                       "instance_ids": np.asarray(list(ids), dtype=np.int64)})
     return b
+
+
+def with_predictor(b: Batch, sigma: float) -> Batch:
+    """The same batch planned with predicted output lengths (a stand-in for the
+    paper's length regressor, Alg. 1's Process 1): o^ = rint(o * e^Z),
+    Z ~ Normal(0, sigma), clipped to [1, generation cap] and to M - s so that
+    every request stays feasible.  Each instance draws from its own stream
+    (its configuration stream with one more word), so samples of a
+    configuration get the same predictions as the full batch."""
+    cfg = int(b.meta["cfg"])
+    ids = b.meta["instance_ids"]
+    cap = CONFIGS[cfg]["o_cap"]
+    plan = np.empty(b.num_requests, dtype=np.int32)
+    for j in range(b.num_instances):
+        lo, hi = int(b.offsets[j]), int(b.offsets[j + 1])
+        rng = np.random.Generator(np.random.PCG64(
+            np.random.SeedSequence([SEED_ROOT[0], SEED_ROOT[1], cfg, int(ids[j]), 1])))
+        o = b.output[lo:hi].astype(np.float64)
+        z = rng.normal(0.0, sigma, hi - lo)
+        hi_cap = np.minimum(cap, b.M - b.prompt[lo:hi].astype(np.int64))
+        plan[lo:hi] = np.clip(np.rint(o * np.exp(z)), 1, hi_cap)
+    out = Batch(b.name + f"+pred{sigma:g}", b.offsets, b.arrival, b.prompt, b.output, b.M,
+                b.policies, long_bit=b.long_bit, plan_len=plan, O0=b.O0, O1=b.O1,
+                meta=dict(b.meta, predictor_sigma=float(sigma)))
+    out.max_steps = default_max_steps(out)
+    return out
 
 
 def tiny_cr_instances(count: int, start: int = 0) -> List[Dict]:

@@ -36,6 +36,18 @@ def test_abi_version():
     assert S.abi_version() == 1
 
 
+def test_policy_codes_match_the_header():
+    src = open(HEADER).read()
+    for name, code in (("SVF_POLICY_FCFS", 0), ("SVF_POLICY_SJF", 1), ("SVF_POLICY_SVF", 2),
+                       ("SVF_POLICY_SVF1BIT", 3), ("SVF_ADMIT_CURRENT", 0x100)):
+        m = re.search(name + r"\s*=\s*(0x[0-9a-fA-F]+|\d+)", src)
+        assert m and int(m.group(1), 0) == code, name
+    assert S.policy_code("svf") == 2 and S.policy_code("fcfs+cur") == 0x100
+    assert S.policy_code("svf1bit+cur") == 0x103
+    with pytest.raises(KeyError):
+        S.policy_code("lifo")
+
+
 def _make(**kw):
     base = dict(offsets=[0, 3], arrival=np.array([0, 1, 1]), prompt=np.array([2, 3, 4]),
                 output=np.array([5, 6, 7]), M=20, policies=["svf"])
@@ -61,6 +73,10 @@ def _make(**kw):
     (dict(max_steps=-1), "SVF_EINVAL", "max_steps"),
     (dict(offsets=[1, 3]), "SVF_EINVAL", "req_offsets[0]"),
     (dict(offsets=[0, 3, 2]), "SVF_EINVAL", "decreases"),
+    # next-step admission lets planned totals pass M: their 32-bit range is checked
+    (dict(offsets=[0, 5], arrival=np.zeros(5), prompt=np.full(5, 2 ** 29 - 2),
+          output=np.ones(5), M=2 ** 29 - 1, policies=["svf+cur"]), "SVF_EINVAL",
+     "SVF_ADMIT_CURRENT"),
 ])
 def test_create_rejects_bad_input(kw, code, text):
     with pytest.raises(S.SvfError) as ei:
@@ -91,6 +107,11 @@ def test_unknown_policy_and_policy_count():
     h = ctypes.c_void_p()
     assert lib.svf_create(ctypes.byref(d), None, ctypes.byref(h)) == -1
     assert b"unknown policy" in lib.svf_last_error()
+    # admission-rule bits other than SVF_ADMIT_CURRENT, and bad base policies under it
+    for code in (0x200 | 2, 0x100 | 4, 0x300, -1):
+        pol[0] = code
+        assert lib.svf_create(ctypes.byref(d), None, ctypes.byref(h)) == -1, code
+        assert b"unknown policy" in lib.svf_last_error()
     d.num_policies = 0
     assert lib.svf_create(ctypes.byref(d), None, ctypes.byref(h)) == -1
     assert lib.svf_create(None, None, ctypes.byref(h)) == -1

@@ -157,6 +157,44 @@ def test_random_ragged(seed):
             compare(b, g[pol], pol, label=f"rand{seed}{kw}")
 
 
+@pytest.mark.parametrize("seed", range(4))
+def test_current_capacity_rule_random(seed):
+    """Next-step admission (Alg. 1's Process 2 read literally) with evictions of
+    requests whose lengths are known, next to the forward-looking rule."""
+    say(f"current-capacity admission, random ragged batches seed {seed}")
+    for kw, pols in ((dict(), ("svf+cur", "sjf+cur", "fcfs+cur", "svf")),
+                     (dict(bits=True), ("svf1bit+cur", "svf+cur", "svf1bit")),
+                     (dict(plan_noise=True), ("svf+cur", "sjf+cur", "sjf"))):
+        b = W.random_small(100 + seed, instances=40, n_max=60, s_max=12, o_max=20, M=60,
+                           gap_mean=[0.0, 0.3, 1.0, 0.1][seed], **kw)
+        b.policies = pols
+        b.max_steps = W.default_max_steps(b)
+        g = gpu_run(b)
+        for pol in pols:
+            compare(b, g[pol], pol, label=f"cur{seed}{kw}")
+        chunked = gpu_run(b, chunks=[1] * 50 + [9, 4, 10 ** 9])
+        for pol in pols:
+            for f in FIELDS:
+                assert np.array_equal(g[pol][f], chunked[pol][f]), (pol, f)
+            assert np.array_equal(g[pol]["stats"], chunked[pol]["stats"]), pol
+
+
+def test_current_capacity_rule_config2_and_config4():
+    pols = ("svf", "svf+cur", "sjf+cur", "fcfs+cur")
+    b = W.config(2, instances=32, policies=pols)
+    say("current-capacity admission: config 2, 32 x 1000")
+    g = gpu_run(b)
+    for pol in pols:
+        compare(b, g[pol], pol, label="cur-cfg2")
+    assert sum(int(g[p]["stats"]["preemptions"].sum()) for p in pols[1:]) > 0
+    b4 = W.config(4, instances=4, policies=("svf", "svf+cur"))
+    say("current-capacity admission: config 4, 4 x 5000")
+    g4 = gpu_run(b4)
+    for pol in b4.policies:
+        compare(b4, g4[pol], pol, label="cur-cfg4")
+    assert int(g4["svf"]["stats"]["preemptions"].sum()) == 0
+
+
 def test_ragged_sizes_with_merge_passes():
     """Instances of very different sizes in one batch: 0, 1, a partial chunk,
     and several chunks of the 8192-element LDS sort joined by merge passes."""
