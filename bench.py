@@ -54,11 +54,19 @@ def traffic_from_profile(workload):
     return d.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg, sample_instances, threads):
-    import oracle
+def make_batch(cfg, instances, policies, sigma):
     from paper_2606_22327_amd import workloads as W
 
-    b = W.config(cfg, instances=sample_instances)
+    b = W.config(cfg, instances=instances, policies=policies)
+    if sigma is not None:
+        b = W.with_predictor(b, sigma)
+    return b
+
+
+def cpu_baseline(cfg, sample_instances, threads, policies=None, sigma=None):
+    import oracle
+
+    b = make_batch(cfg, sample_instances, policies, sigma)
     t0 = time.perf_counter()
     rs = 0
     for pol in b.policies:
@@ -77,6 +85,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--instances", type=int, default=None)
+    ap.add_argument("--policies", default=None,
+                    help="comma-separated policy names instead of the workload's own "
+                         "(suffix +cur: admission on the next step's memory only)")
+    ap.add_argument("--predictor-sigma", type=float, default=None,
+                    help="plan with predicted lengths o * LogNormal(0, sigma), rounded")
     ap.add_argument("--cpu-sample", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -96,7 +109,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     t0 = time.perf_counter()
-    batch = W.config(args.config, instances=args.instances)
+    policies = tuple(args.policies.split(",")) if args.policies else None
+    batch = make_batch(args.config, args.instances, policies, args.predictor_sigma)
     log(f"generated {W.CONFIG_TITLES[args.config]}: {batch.num_requests} requests "
         f"in {time.perf_counter() - t0:.1f}s")
     t0 = time.perf_counter()
@@ -149,6 +163,10 @@ def main():
     sim_avg_s = tm["sim_ms"] / max(1, tm["sim_launches"]) / 1000.0
     achieved = b_alg / sim_avg_s / 1e9
     workload = f"cfg{args.config}"
+    if policies or args.predictor_sigma is not None:
+        workload += "-" + "-".join(batch.policies).replace("+", "")
+        if args.predictor_sigma is not None:
+            workload += f"-sigma{args.predictor_sigma:g}"
     traffic = traffic_from_profile(workload)
 
     out = {
@@ -164,7 +182,10 @@ def main():
         "vs_baseline": None,
         "dtype": "int32/int64",
         "data": "synthetic",
-        "config": {"workload": W.CONFIG_TITLES[args.config], "instances": batch.num_instances,
+        "config": {"workload": W.CONFIG_TITLES[args.config]
+                   + (f", predicted lengths (sigma {args.predictor_sigma:g})"
+                      if args.predictor_sigma is not None else ""),
+                   "instances": batch.num_instances,
                    "requests": batch.num_requests, "policies": list(batch.policies),
                    "M": batch.M, "request_steps_per_step": req_steps,
                    "all_instances_done": status_ok},
@@ -178,7 +199,8 @@ def main():
     if not args.no_cpu_baseline:
         threads = min(os.cpu_count() or 1, 16)
         log(f"cpu baseline: oracle on {args.cpu_sample} instances, {threads} threads")
-        out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample, threads)
+        out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample, threads, policies,
+                                           args.predictor_sigma)
         out["cpu_baseline"]["host"] = platform.processor() or platform.machine()
     print(json.dumps(out))
 

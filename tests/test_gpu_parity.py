@@ -195,6 +195,29 @@ def test_current_capacity_rule_config2_and_config4():
     assert int(g4["svf"]["stats"]["preemptions"].sum()) == 0
 
 
+def test_predictor_in_the_loop_config2_and_config4():
+    """Plans from a noisy length predictor (o * LogNormal(0, sigma)): requests
+    outrun their plans, get evicted and restart; plans that never undershoot
+    never evict."""
+    b = W.with_predictor(W.config(2, instances=32, policies=("svf", "sjf", "fcfs", "svf+cur")),
+                         0.5)
+    say("predicted lengths: config 2, 32 x 1000, sigma 0.5")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="pred-cfg2")
+    assert int(g["svf"]["stats"]["preemptions"].sum()) > 0
+    b.plan_len = np.maximum(b.plan_len, b.output).astype(np.int32)
+    b.policies = ("svf", "sjf", "fcfs")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="pred-over-cfg2")
+        assert int(g[pol]["stats"]["preemptions"].sum()) == 0
+    b4 = W.with_predictor(W.config(4, instances=4), 0.5)
+    say("predicted lengths: config 4, 4 x 5000, sigma 0.5")
+    g4 = gpu_run(b4)
+    compare(b4, g4["svf"], "svf", label="pred-cfg4")
+
+
 def test_ragged_sizes_with_merge_passes():
     """Instances of very different sizes in one batch: 0, 1, a partial chunk,
     and several chunks of the 8192-element LDS sort joined by merge passes."""
@@ -372,3 +395,22 @@ def test_full_config5_against_stored_oracle_digests():
         for f in SFIELDS:
             assert int(g["stats"][f][i]) == ent["stats"][f], (i, f)
     properties(b, g, "svf")
+
+
+def test_full_config4_predictor_sampled():
+    """The full heavy-traffic workload planned with predicted lengths (sigma
+    0.5), in one launch: sampled instances against the oracle, every instance
+    through properties that hold with preemption."""
+    b = W.with_predictor(W.config(4), 0.5)
+    say(f"full config 4 with predicted lengths: {b.num_instances} instances")
+    t0 = time.time()
+    g = gpu_run(b)
+    say(f"gpu done in {time.time() - t0:.1f}s")
+    st = g["svf"]["stats"]
+    assert (st["status"] == 0).all()
+    assert (g["svf"]["finish"] == g["svf"]["start"] + b.output).all()
+    assert (g["svf"]["start"] >= b.arrival).all()
+    assert (st["peak_mem"] <= b.M).all()
+    assert int(st["preemptions"].sum()) == int(g["svf"]["preempt"].sum()) > 0
+    ids = [0, 1, 4095, 8191, 12000, b.num_instances - 1]
+    compare(b, g["svf"], "svf", ids=ids, label="pred-full-cfg4")

@@ -404,3 +404,55 @@ def test_current_capacity_preempts_where_lookahead_does_not():
     cur = oracle.run(b, "svf+cur")
     assert int(la["stats"][:, 5].sum()) == 0
     assert int(cur["stats"][:, 5].sum()) > 0
+
+
+def test_predicted_lengths_that_never_undershoot_never_preempt():
+    """With o^ >= o the planned profile bounds the true one from above, so the
+    forward-looking check keeps the true memory <= M and no eviction ever
+    fires; the schedule is then fixed by the validator with the believed
+    lengths (early finishers release their planned future at their true
+    finish)."""
+    b = W.with_predictor(W.config(2, instances=6, n=300), 0.6)
+    b.plan_len = np.maximum(b.plan_len, b.output).astype(np.int32)
+    assert (b.plan_len > b.output).any()
+    for pol in ("svf", "sjf", "fcfs"):
+        r = oracle.run(b, pol)
+        assert int(r["stats"][:, 5].sum()) == 0
+        for i in range(b.num_instances):
+            lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+            d = b.instance(i)
+            validate.validate(d["arrival"], d["prompt"], d["output"], r["start"][lo:hi],
+                              r["admit_seq"][lo:hi], b.M, pol, ohat=d["plan_len"],
+                              finish=r["finish"][lo:hi])
+
+
+def test_predictor_with_zero_noise_is_the_known_length_run():
+    b = W.config(2, instances=4, n=300)
+    bp = W.with_predictor(b, 0.0)
+    assert np.array_equal(bp.plan_len, b.output)
+    for pol in ("svf", "sjf", "fcfs"):
+        r1, r2 = oracle.run(b, pol), oracle.run(bp, pol, max_steps=b.max_steps)
+        for f in ("start", "finish", "preempt", "admit_seq"):
+            assert np.array_equal(r1[f], r2[f]), (pol, f)
+
+
+def test_c_oracle_matches_literal_with_predicted_lengths():
+    """Underestimates make requests run past their plan and force evictions;
+    the C oracle and the literal simulator must agree step for step."""
+    b = W.with_predictor(W.config(1, instances=6), 0.7)
+    pre = 0
+    for pol in ("svf", "sjf", "fcfs", "svf+cur"):
+        r = oracle.run(b, pol)
+        for i in range(b.num_instances):
+            lo, hi = int(b.offsets[i]), int(b.offsets[i + 1])
+            d = b.instance(i)
+            L = literal.simulate(d["arrival"], d["prompt"], d["output"], b.M, pol,
+                                 plan=d["plan_len"], max_steps=b.max_steps)
+            for f in ("start", "finish", "preempt", "admit_seq"):
+                assert list(r[f][lo:hi]) == L[f], (pol, i, f)
+            row = r["stats"][i]
+            for c, f in enumerate(oracle.STAT_FIELDS):
+                if f in L:
+                    assert int(row[c]) == L[f], (pol, i, f)
+            pre += L["preemptions"]
+    assert pre > 0

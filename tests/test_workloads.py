@@ -101,3 +101,24 @@ def test_random_small_is_ragged_and_feasible():
     sizes = np.diff(b.offsets)
     assert sizes[0] == 0 and sizes[1] == 1
     assert int((b.prompt + np.maximum(b.output, max(b.O0, b.O1))).max()) <= b.M
+
+
+def test_predictor_plans_are_feasible_seeded_and_unbiased_in_log():
+    b = W.config(2, instances=40, n=500)
+    for sigma in (0.25, 0.8):
+        p = W.with_predictor(b, sigma)
+        cap = np.minimum(W.CONFIGS[2]["o_cap"], b.M - b.prompt.astype(np.int64))
+        assert (p.plan_len >= 1).all() and (p.plan_len <= cap).all()
+        assert np.array_equal(p.output, b.output) and p.plan_len.dtype == np.int32
+        # the same instances drawn on their own get the same predictions
+        q = W.with_predictor(W.config(2, instances=[5, 17], n=500), sigma)
+        assert np.array_equal(q.plan_len, p.subset([5, 17]).plan_len)
+        assert np.array_equal(p.subset([5, 17]).plan_len,
+                              W.with_predictor(b.subset([5, 17]), sigma).plan_len)
+        # log-ratio: centred, spread close to sigma (requests away from the clips)
+        o = b.output.astype(np.float64)
+        mid = (o >= 20) & (o * np.exp(3 * sigma) < cap)
+        lr = np.log(p.plan_len[mid] / o[mid])
+        assert abs(float(np.median(lr))) < 0.05
+        assert abs(float(lr.std()) - sigma) < 0.1 * sigma
+        assert p.max_steps == 64 * b.max_steps  # room for lost progress
