@@ -66,3 +66,43 @@ def poisson_conditional_proxies(mu: float, theta: int):
     q = 1.0 - mu
     r = theta * q ** theta / (1.0 - q ** theta)
     return 1.0 / mu - r, theta + 1.0 / mu, 0.5 * r * r
+
+
+# ---- Poisson arrivals, geometric outputs (Section 3.3; proofs in the appendix
+#      on the stochastic bounds).  q = 1 - mu; alpha = max (s + o) / M;
+#      C = (1 - alpha) M / 2 is the processing rate of Lemma 1 there.
+
+def poisson_capacity(M: float, alpha: float) -> float:
+    """Lemma 1 of the stochastic appendix: with a non-empty queue the rate of
+    processed volume exceeds (1 - alpha) M / 2."""
+    return (1.0 - alpha) * M / 2.0
+
+
+def poisson_rho(lam: float, mean_vol: float, M: float, alpha: float) -> float:
+    """Worst-case utilisation rho = lam E[vol] / ((1 - alpha) M / 2)."""
+    return lam * mean_vol / poisson_capacity(M, alpha)
+
+
+def poisson_w0(lam: float, mean_s: float, mu: float) -> float:
+    """Lemma 2 of the stochastic appendix: W_0 = lam (E[s]/mu^2 + 2/mu^3)."""
+    return lam * (mean_s / mu ** 2 + 2.0 / mu ** 3)
+
+
+def poisson_w_exact(lam: float, mean_s: float, mu: float) -> float:
+    """W_exact = (1 - mu) W_0 (end of the proof of thm:svf_poisson)."""
+    return (1.0 - mu) * poisson_w0(lam, mean_s, mu)
+
+
+def poisson_svf_latency_bound(lam, mean_s, mu, M, alpha, distortion=1.0):
+    """The step of the proof before OPT enters: E[latency] <= E[o] + factor *
+    W_0 / ((1 - alpha) M / 2 - lam E[vol]), factor = 1 for SVF and
+    E[vol] / (E[vol] - eps) for 1-bit SVF."""
+    ev = geometric_mean_volume(mean_s, mu)
+    slack = poisson_capacity(M, alpha) - lam * ev
+    return 1.0 / mu + distortion * poisson_w0(lam, mean_s, mu) / slack
+
+
+def poisson_cr_bound(alpha: float, mu: float, rho: float, distortion: float = 1.0) -> float:
+    """Theorems thm:svf_poisson (distortion 1) and thm:svf_1bit_poisson
+    (distortion E[vol] / (E[vol] - eps)): 1 + d * 2 / ((1-alpha)(1-mu)(1-rho))."""
+    return 1.0 + distortion * 2.0 / ((1.0 - alpha) * (1.0 - mu) * (1.0 - rho))

@@ -456,3 +456,95 @@ def test_c_oracle_matches_literal_with_predicted_lengths():
                     assert int(row[c]) == L[f], (pol, i, f)
             pre += L["preemptions"]
     assert pre > 0
+
+
+# ------------------------------------------- stochastic bounds (Section 3.3)
+
+def _geo_pmf(mu, kmax):
+    k = np.arange(1, kmax + 1, dtype=np.float64)
+    return k, mu * (1.0 - mu) ** (k - 1)
+
+
+@pytest.mark.parametrize("mu,theta", [(1 / 50, 10), (1 / 50, 80), (1 / 200, 200), (0.3, 3)])
+def test_conditional_mean_proxies_and_distortion_by_summation(mu, theta):
+    """Theorem thm:svf_1bit_poisson: O_0 and O_1 are E[o | o <= theta] and
+    E[o | o > theta]; eps = E[Delta] - min Delta with Delta_m = E[(o^2+o)/2 | m]
+    - (O_m^2 + O_m)/2, all summed over the geometric law directly."""
+    O0, O1, eps = bounds.poisson_conditional_proxies(mu, theta)
+    k, p = _geo_pmf(mu, int(60 / mu) + 10 * theta)
+    short = k <= theta
+    p1, p2 = p[short].sum(), p[~short].sum()
+    e_short = (k[short] * p[short]).sum() / p1
+    e_long = (k[~short] * p[~short]).sum() / p2
+    assert O0 == pytest.approx(e_short, rel=1e-9)
+    assert O1 == pytest.approx(e_long, rel=1e-9)
+    half = (k * k + k) / 2
+    d1 = (half[short] * p[short]).sum() / p1 - (O0 * O0 + O0) / 2
+    d2 = (half[~short] * p[~short]).sum() / p2 - (O1 * O1 + O1) / 2
+    assert d2 == pytest.approx((1 - mu) / (2 * mu * mu), rel=1e-7)   # memoryless tail
+    assert d1 < d2
+    assert eps == pytest.approx(p1 * d1 + p2 * d2 - min(d1, d2), rel=1e-6)
+
+
+def test_lemma2_residual_volume_and_w0_by_summation():
+    """Lemma 2 of the stochastic appendix: a running request holding m tokens
+    with Geometric(mu) remaining length R leaves E[m R + (R + R^2)/2] =
+    m/mu + 1/mu^2 of volume; with E[M(t)] = lam E[vol] and E[N(t)] = lam/mu
+    this is W_0 = lam E[vol]/mu + lam/mu^3 = lam (E[s]/mu^2 + 2/mu^3)."""
+    mu, lam, m, es = 1 / 40, 0.37, 123.0, 77.5
+    k, p = _geo_pmf(mu, 4000)
+    assert float((p * (m * k + (k + k * k) / 2)).sum()) == pytest.approx(m / mu + 1 / mu ** 2,
+                                                                        rel=1e-9)
+    ev = float((p * (es * k + (k * k + k) / 2)).sum())
+    assert ev == pytest.approx(bounds.geometric_mean_volume(es, mu), rel=1e-9)
+    assert bounds.poisson_w0(lam, es, mu) == pytest.approx(lam * ev / mu + lam / mu ** 3,
+                                                           rel=1e-9)
+    assert bounds.poisson_w_exact(lam, es, mu) == pytest.approx(
+        (1 - mu) * bounds.poisson_w0(lam, es, mu))
+
+
+def test_priority_queue_recursion_closed_forms():
+    """The proof of thm:svf_poisson solves W(v) D(v+1) = W_0 + sum_{x<v}
+    lam_x x W(x), D(v) = C - sum_{x<v} lam_x x, in closed form
+    W(v) = D(1) W_0 / (D(v) D(v+1)) with sum_v lam_v v W(v) =
+    W_0 (D(1)/D(inf) - 1); the 1-bit proof telescopes the same sum over classes.
+    Both are checked against the recursion solved step by step."""
+    rng = np.random.default_rng(5)
+    V, C, W0 = 60, 1000.0, 3.7
+    lamx = rng.random(V) * 0.3
+    lamx *= 0.8 * C / float((lamx * np.arange(1, V + 1)).sum())   # load 0.8 C
+    D = C - np.concatenate([[0.0], np.cumsum(lamx * np.arange(1, V + 1))])  # D[v-1] = D(v)
+    W = np.zeros(V + 1)
+    acc = 0.0
+    for v in range(1, V + 1):
+        W[v] = (W0 + acc) / D[v]          # D(v+1) is D[v]
+        acc += lamx[v - 1] * v * W[v]
+    for v in range(1, V + 1):
+        assert W[v] == pytest.approx(D[0] * W0 / (D[v - 1] * D[v]), rel=1e-10)
+    assert acc == pytest.approx(W0 * (D[0] / D[V] - 1), rel=1e-10)
+    # the class form: sum_k (R_k - R_{k-1}) / ((C - R_{k-1})(C - R_k)) telescopes
+    R = np.concatenate([[0.0], np.cumsum(rng.random(7) * 100)])
+    lhs = float(((R[1:] - R[:-1]) / ((C - R[:-1]) * (C - R[1:]))).sum())
+    assert lhs == pytest.approx(1 / (C - R[-1]) - 1 / C, rel=1e-12)
+
+
+def test_poisson_bounds_shape():
+    """rho < 1 keeps the bounds finite; they grow with rho and with the
+    distortion factor; at rho -> 0 the latency bound tends to E[o]."""
+    mu, es, M, alpha = 1 / 200, 256.5, 65536, (512 + 3000) / 65536
+    ev = bounds.geometric_mean_volume(es, mu)
+    prev = 0.0
+    for rho in (0.1, 0.5, 0.9, 0.99):
+        lam = rho * bounds.poisson_capacity(M, alpha) / ev
+        assert bounds.poisson_rho(lam, ev, M, alpha) == pytest.approx(rho)
+        b = bounds.poisson_cr_bound(alpha, mu, rho)
+        assert b > prev and b > 1 + 2 / (1 - alpha)
+        prev = b
+        lat = bounds.poisson_svf_latency_bound(lam, es, mu, M, alpha)
+        lat1 = bounds.poisson_svf_latency_bound(lam, es, mu, M, alpha, distortion=1.1)
+        assert 1 / mu < lat < lat1
+    assert bounds.poisson_svf_latency_bound(1e-9, es, mu, M, alpha) == pytest.approx(1 / mu)
+    _, _, e200 = bounds.poisson_conditional_proxies(mu, 200)
+    _, _, e600 = bounds.poisson_conditional_proxies(mu, 600)
+    _, _, e1000 = bounds.poisson_conditional_proxies(mu, 1000)
+    assert e1000 < e600 < e200 < ev
