@@ -95,6 +95,12 @@ def load(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"libsvfsim.so is not built ({path}); run __graft_entry__.build()")
+    # torch ships its own HIP runtime; loading it before this library (which
+    # links the system one) is the order in which both work in one process.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     lib.svf_create.argtypes = [ctypes.POINTER(BatchDesc), V, ctypes.POINTER(V)]

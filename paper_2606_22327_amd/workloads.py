@@ -290,6 +290,32 @@ def with_predictor(b: Batch, sigma: float) -> Batch:
     return out
 
 
+def poisson_geometric(lam: float, mu: float, s_max: int, o_cap: int, M: int, n: int,
+                      instances: int, tag: int = 0, policies=("svf",), theta: int = 0,
+                      O0: int = 0, O1: int = 0, first: int = 0) -> Batch:
+    """The stochastic model of the Poisson-arrival theorems (Section 3.3):
+    arrivals of rate ``lam`` per step (continuous Poisson process read off at
+    integer steps), prompts uniform on {1..s_max}, outputs Geometric(mu) on
+    {1, 2, ...} clipped at ``o_cap`` (so s + o <= s_max + o_cap; the clipped
+    mass is (1 - mu)^o_cap).  ``theta`` > 0 adds the exact 1-bit labels
+    b = [o > theta] with proxies O0, O1 given by the caller.  Instance i draws
+    from its own stream (``tag`` separates parameter sets)."""
+    parts = []
+    for i in range(first, first + instances):
+        rng = np.random.Generator(np.random.PCG64(
+            np.random.SeedSequence([SEED_ROOT[0], SEED_ROOT[1], 6, int(tag), int(i)])))
+        a = _poisson_arrivals(rng, 1.0 / lam, n)
+        s_ = _uniform(rng, 1, s_max, n)
+        o = np.minimum(rng.geometric(mu, size=n), o_cap).astype(np.int64)
+        d = {"arrival": a, "prompt": s_, "output": o}
+        if theta > 0:
+            d["long_bit"] = (o > theta).astype(np.int8)
+        parts.append(d)
+    return assemble(f"poisson-geo{tag}", parts, M, tuple(policies), O0=O0, O1=O1,
+                    meta={"lam": lam, "mu": mu, "s_max": s_max, "o_cap": o_cap,
+                          "theta": theta, "tag": tag, "first": first})
+
+
 def tiny_cr_instances(count: int, start: int = 0) -> List[Dict]:
     """Configuration 0: tiny burst instances with their own budgets."""
     return [gen_instance(0, i) for i in range(start, start + count)]

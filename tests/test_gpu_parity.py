@@ -414,3 +414,22 @@ def test_full_config4_predictor_sampled():
     assert int(st["preemptions"].sum()) == int(g["svf"]["preempt"].sum()) > 0
     ids = [0, 1, 4095, 8191, 12000, b.num_instances - 1]
     compare(b, g["svf"], "svf", ids=ids, label="pred-full-cfg4")
+
+
+def test_poisson_geometric_bounds_and_parity():
+    """The stochastic model of Section 3.3 on the GPU: sampled instances
+    against the oracle, and the measured mean latency against the bounds of
+    thm:svf_poisson and thm:svf_1bit_poisson where they apply (rho < 1)."""
+    from paper_2606_22327_amd import stochastic as ST
+    model = ST.Model()
+    say("poisson/geometric: rho 0.5, 0.9, 2.0; 16 x 4000 per setting")
+    rows = ST.run(model, (0.5, 0.9, 2.0), instances=16, n=4000, tag=7, keep_outputs=True)
+    assert len(rows) == 3 * 5
+    for r in rows:
+        b, out = r.extra["batch"], r.extra["out"]
+        compare(b, dict(out, stats=r.extra["stats"]), r.policy, ids=[0, 9, 15],
+                label=f"poisson rho={r.rho} {r.policy} th={r.theta}")
+        assert r.ratio >= 1.0
+        if r.rho < 1 and r.policy in ("svf", "svf1bit"):
+            assert r.mean_latency <= r.latency_bound, r
+            assert r.ratio <= r.cr_bound, r
