@@ -1,7 +1,8 @@
 """Build the HIP library ``libsvfsim.so`` for gfx950 with hipcc.
 
 The library holds every kernel of the simulator and the host runtime behind
-the C ABI of ``include/svfsim.h``.  It is built in-tree so that the same file
+the C ABI of ``include/svfsim.h``, plus the host-side exact optimum of tiny
+burst instances (``include/svfopt.h``).  It is built in-tree so that the same file
 is loaded by the tests, the smoke check and the benchmark.
 """
 
@@ -32,9 +33,12 @@ def build(verbose: bool = False) -> str:
     rt_o = os.path.join(BUILD, "svf_runtime.o")
     _run(["hipcc", f"--offload-arch={ARCH}", *COMMON, *GPU_FLAGS, "-c",
           os.path.join(CSRC, "svf_kernels.hip"), "-o", kern_o])
+    opt_o = os.path.join(BUILD, "svf_opt.o")
     _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "svf_runtime.cpp"), "-o", rt_o])
+    _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "svf_opt.cpp"), "-o", opt_o])
     tmp = LIB + ".tmp"
-    _run(["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_o, rt_o, "-o", tmp])
+    _run(["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_o, rt_o, opt_o, "-pthread",
+          "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:
         print(LIB)

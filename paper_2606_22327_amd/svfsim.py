@@ -31,13 +31,13 @@ def policy_code(name: str) -> int:
         return POLICY[name[:-4]] | ADMIT_CURRENT
     return POLICY[name]
 ERRORS = {0: "SVF_OK", -1: "SVF_EINVAL", -2: "SVF_ENOMEM", -3: "SVF_EHIP",
-          -4: "SVF_EINFEASIBLE", -5: "SVF_ESTATE"}
+          -4: "SVF_EINFEASIBLE", -5: "SVF_ESTATE", -6: "SVF_ELIMIT"}
 STATUS = {0: "done", 1: "exhausted", 2: "running"}
 
 # every symbol the header declares
 EXPORTS = ("svf_create", "svf_reset", "svf_step", "svf_run", "svf_read", "svf_stats",
            "svf_set_profiling", "svf_timings", "svf_shape", "svf_destroy",
-           "svf_last_error", "svf_abi_version")
+           "svf_last_error", "svf_abi_version", "svf_opt_burst", "svf_opt_burst_batch")
 
 
 class SvfError(RuntimeError):
@@ -116,6 +116,8 @@ def load(path: str = LIB_PATH):
     lib.svf_last_error.argtypes = []
     lib.svf_last_error.restype = ctypes.c_char_p
     lib.svf_abi_version.argtypes = []
+    lib.svf_opt_burst.argtypes = [I32, V, V, I64, I64, ctypes.POINTER(I64), ctypes.POINTER(I64)]
+    lib.svf_opt_burst_batch.argtypes = [I32, V, V, V, V, I64, I32, V, V, V]
     for name in EXPORTS:
         if name not in ("svf_last_error",):
             getattr(lib, name).restype = ctypes.c_int
@@ -292,3 +294,42 @@ def abi_version() -> int:
 
 def last_error() -> str:
     return load().svf_last_error().decode(errors="replace")
+
+
+def opt_burst(prompt, output, M: int, state_limit: int = 0):
+    """Exact optimal total latency of one burst instance (host code; see
+    svfopt.h).  Returns (total latency, states stored)."""
+    lib = load()
+    s = np.ascontiguousarray(prompt, dtype=np.int32)
+    o = np.ascontiguousarray(output, dtype=np.int32)
+    tot, st = ctypes.c_int64(), ctypes.c_int64()
+    rc = lib.svf_opt_burst(len(s), _host_ptr(s), _host_ptr(o), int(M), int(state_limit),
+                           ctypes.byref(tot), ctypes.byref(st))
+    if rc != 0:
+        raise SvfError(rc, f"svf_opt_burst failed ({st.value} states)")
+    return int(tot.value), int(st.value)
+
+
+def opt_burst_batch(offsets, prompt, output, M, threads: int = 0, state_limit: int = 0):
+    """Exact optima of many burst instances (CSR ``offsets``, per-instance
+    budgets ``M``) on host threads (0: up to 16).  Returns (totals, states, status);
+    status[i] != 0 marks an instance that was not solved (totals[i] = -1)."""
+    lib = load()
+    if threads <= 0:
+        threads = min(16, os.cpu_count() or 1)
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    s = np.ascontiguousarray(prompt, dtype=np.int32)
+    o = np.ascontiguousarray(output, dtype=np.int32)
+    m = np.ascontiguousarray(M, dtype=np.int64)
+    n = len(off) - 1
+    assert m.shape == (n,)
+    tot = np.full(n, -1, dtype=np.int64)
+    st = np.zeros(n, dtype=np.int64)
+    status = np.zeros(n, dtype=np.int32)
+    rc = lib.svf_opt_burst_batch(n, _host_ptr(off), _host_ptr(s), _host_ptr(o), _host_ptr(m),
+                                 int(state_limit), int(threads), _host_ptr(tot), _host_ptr(st),
+                                 _host_ptr(status))
+    if rc != 0 and (status == 0).all():   # an argument error, not a per-instance one
+        raise SvfError(rc, "svf_opt_burst_batch failed")
+    tot[status != 0] = -1
+    return tot, st, status

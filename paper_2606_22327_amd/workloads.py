@@ -321,6 +321,25 @@ def tiny_cr_instances(count: int, start: int = 0) -> List[Dict]:
     return [gen_instance(0, i) for i in range(start, start + count)]
 
 
+def tiny_alpha_instances(k: int, count: int, n_lo: int, n_hi: int, s_max: int, o_max: int,
+                         tag: int = 0) -> Batch:
+    """Burst instances for a competitive-ratio sweep at alpha = 1/k: n drawn
+    from {n_lo..n_hi}, s from {1..s_max}, o from {1..o_max}; request 0 is the
+    largest possible one (s_max, o_max), and every instance shares the budget
+    M = k (s_max + o_max), so max_i (s_i + o_i) / M = 1/k exactly."""
+    parts = []
+    for i in range(count):
+        rng = np.random.Generator(np.random.PCG64(
+            np.random.SeedSequence([SEED_ROOT[0], SEED_ROOT[1], 7, int(k), int(tag), int(i)])))
+        n = int(_uniform(rng, n_lo, n_hi, 1)[0])
+        s_ = _uniform(rng, 1, s_max, n)
+        o = _uniform(rng, 1, o_max, n)
+        s_[0], o[0] = s_max, o_max
+        parts.append({"arrival": np.zeros(n, dtype=np.int64), "prompt": s_, "output": o})
+    return assemble(f"alpha1/{k}", parts, k * (s_max + o_max), ("svf", "sjf", "fcfs"),
+                    meta={"k": k, "s_max": s_max, "o_max": o_max, "tag": tag})
+
+
 def random_small(seed: int, instances: int, n_max: int, s_max: int, o_max: int,
                  M: int, gap_mean: float = 0.0, bits: bool = False,
                  plan_noise: bool = False, ragged: bool = True) -> Batch:

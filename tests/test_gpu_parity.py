@@ -433,3 +433,31 @@ def test_poisson_geometric_bounds_and_parity():
         if r.rho < 1 and r.policy in ("svf", "svf1bit"):
             assert r.mean_latency <= r.latency_bound, r
             assert r.ratio <= r.cr_bound, r
+
+
+def test_cr_sweep_and_search():
+    """Tiny burst instances at several alpha: the GPU's total latencies equal
+    the oracle's, each policy is at or above the exact optimum, and SVF stays
+    within 1 + 2/(1 - alpha) (Theorem thm:svf-burst), also on the instances
+    an evolutionary search drives towards a large ratio."""
+    from oracle import opt
+    from paper_2606_22327_amd import crsweep as CR
+    say("competitive-ratio sweep: alpha 1/2, 1/4, 1/10; 256 instances each")
+    for k in (2, 4, 10):
+        b = W.tiny_alpha_instances(k, 256, 6, 10, 4, 6, tag=9)
+        g = gpu_run(b)
+        for pol in b.policies:
+            compare(b, g[pol], pol, label=f"alpha1/{k}")
+        r = CR.sweep([k], 256, n_hi=10, tag=9)[0]
+        for pol in CR.POLICIES:
+            assert r.mean_ratio[pol] >= 1.0
+        assert r.max_ratio["svf"] <= r.bound
+    say("evolutionary search at alpha 1/2: 64 members, 4 generations")
+    res = CR.search(2, population=64, generations=4, n_hi=8, threads=8)
+    assert 1.0 <= res.max_ratio["svf"] <= res.bound
+    s, o = res.worst["svf"]
+    want = opt.optimal_total_latency(s, o, res.M)
+    bw = W.assemble("worst", [{"arrival": np.zeros(len(s)), "prompt": np.array(s),
+                               "output": np.array(o)}], res.M, ("svf",))
+    tel = int(oracle.run(bw, "svf")["stats"][0, 2])
+    assert tel / want == pytest.approx(res.max_ratio["svf"])
