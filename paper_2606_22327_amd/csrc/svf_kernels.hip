@@ -10,7 +10,8 @@
 //                     the partner run)
 //   k_build_rec       rank-ordered request records and the index->rank map
 //   k_sim<D_LDS>      the simulation: one wave64 per segment
-//   k_finalize        per-request outputs as of the reached step + per-segment
+//   k_finalize        per-request outputs as of the reached step (finish derived
+//                     as start + o where lengths are known) + per-segment
 //                     statistics
 //
 // Waiting set.  A segment's requests are sorted once by priority; the waiting
@@ -645,6 +646,19 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     };
     int4 hq = make_int4(0, 0, 0, 0);  // record of the blocked head
     if (head >= 0) hq = rec_of(head);
+    // Admissions are staged in registers, lane j holding the j-th of up to 64
+    // (request index and start step), and written out 64 at a time with their
+    // admission numbers, so that no store is in flight behind each admission;
+    // the finish (start + o) is derived when the outputs are finalised.
+    int stg_idx = 0, stg_t = 0, nstg = 0, seq0 = seq;
+    auto flush = [&]() {
+        if (lane < nstg) {
+            sg.start[stg_idx] = stg_t;
+            sg.admit_seq[stg_idx] = seq0 + lane;
+        }
+        seq0 += nstg;
+        nstg = 0;
+    };
 
     // Bitmap word of the current candidate, mirrored in scalar registers for
     // the admission loop of one step (nothing else writes the bitmap there).
@@ -664,18 +678,29 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
         if (t >= t_lim) break;
 
-        // 1. arrivals: a prefix of the window (arrivals are sorted)
-        int new_min = INT32_MAX;
+        // 1. arrivals: a prefix of the window (arrivals are sorted).  n_below
+        //    counts those ranked above the blocked head (the lowest waiting
+        //    rank before this step; none if nothing was waiting).
+        const int old_head = head < 0 ? INT32_MAX : head;
+        const int4 hq0 = hq;
+        int new_min = INT32_MAX, n_below = 0;
         int4 nq = make_int4(0, 0, 0, 0);
         for (;;) {
             const bool arr = (wb + lane >= cursor) && (a_reg == t);
             const uint64_t m = ballot(arr);
             if (m == 0ull) break;
             if (arr) bitmap_set_atomic(B, S, rk_reg);
-            const int mn = wmin(arr ? rk_reg : INT32_MAX);
+            n_below += __popcll(ballot(arr && rk_reg < old_head));
+            int mn, src;
+            if ((m & (m - 1ull)) == 0ull) {  // a single arrival
+                src = __builtin_ctzll(m);
+                mn = __builtin_amdgcn_readlane(rk_reg, src);
+            } else {
+                mn = wmin(arr ? rk_reg : INT32_MAX);
+                src = __builtin_ctzll(ballot(arr && rk_reg == mn));
+            }
             if (mn < new_min) {
                 new_min = mn;
-                const int src = __builtin_ctzll(ballot(arr && rk_reg == mn));
                 nq = readlane4(aq, src);
             }
             cursor += __popcll(m);
@@ -685,12 +710,10 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         lds_order();
 
         // 4. admissions (known lengths: completions change nothing ahead)
-        // (head < 0 means nothing was waiting before this step's arrivals)
-        const int head_eff = head < 0 ? INT32_MAX : head;
-        if (new_min < head_eff || (head >= 0 && t >= t_f)) {
+        if (new_min < old_head || (head >= 0 && t >= t_f)) {
             int r = head;
             int4 q = hq;
-            if (new_min < head_eff) { r = new_min; q = nq; }
+            if (new_min < old_head) { r = new_min; q = nq; }
             load_word(r >> 6);  // arrivals may have changed any word
             for (;;) {
                 int tf = 0;
@@ -701,18 +724,32 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                     folded = to;
                 }
                 if (!fit_and_admit(D, t, q.y, q.z, M, 0, max_fin, &tf)) { head = r; hq = q; t_f = tf; break; }
+                if (lane == nstg) {
+                    stg_idx = q.x;
+                    stg_t = t;
+                }
+                if (++nstg == 64) flush();
                 cbits &= ~(1ull << (r & 63));
                 if (lane == 0) {
                     B[cw] = cbits;
                     if (cbits == 0ull) S[cw >> 6] &= ~(1ull << (cw & 63));
-                    sg.start[q.x] = t;
-                    sg.admit_seq[q.x] = seq;
-                    sg.fin[q.x] = t + q.w;
                 }
                 lds_order();
                 ++seq;
                 ++nadm;
                 max_fin = max(max_fin, t + q.w);
+                // Once every arrival ranked above the old head is running, the
+                // old head (record known) is next, or nothing is left waiting.
+                // Before t_f it still does not fit: the profile has only grown
+                // since t_f was computed, which can only delay the release.
+                if (r < old_head && --n_below == 0) {
+                    if (old_head == INT32_MAX) { head = -1; break; }
+                    if (t < t_f) break;
+                    r = old_head;
+                    q = hq0;
+                    if (cw != (r >> 6)) load_word(r >> 6);
+                    continue;
+                }
                 if (cbits != 0ull) {
                     r = cw * 64 + __builtin_ctzll(cbits);
                 } else {
@@ -737,6 +774,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         if (nt <= t) nt = t + 1;
         t = uni(nt);
     }
+    flush();
     // every past step folded: the ring is canonical again and the peak complete
     fold_range(D, folded, t, peak_lane);
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nadm; st.max_fin = max_fin;
@@ -987,7 +1025,8 @@ __global__ __launch_bounds__(64) void k_finalize(FinArgs F) {
     int mk = 0;
     for (int j = lane; j < n; j += 64) {
         const int k = F.start[base + j];
-        int f = F.fin[base + j];
+        // known lengths: the finish is start + o (not stored by the simulation)
+        int f = stepped ? F.fin[base + j] : (k >= 0 ? k + F.o[off + j] : -1);
         if (f > t_end - 1) f = -1;
         F.fin_out[base + j] = f;
         if (f >= 0) {
