@@ -58,6 +58,11 @@ struct SortArgs {
     int64_t N;
     int32_t O0, O1;
     int32_t CH;
+    int32_t kbits[8];         // [P] bits of the largest priority key of each policy
+    int32_t* start;           // [P*N] outputs cleared by the fused sort (k_sort_rec)
+    int32_t* fin;
+    int32_t* preempt;
+    int32_t* admit_seq;
 };
 
 struct SimArgs {
@@ -109,6 +114,11 @@ hipError_t launch_init_state(SegState* st, int32_t G, hipStream_t s);
 hipError_t launch_chunk_sort(const SortArgs& A, int nchunks, hipStream_t s);
 hipError_t launch_merge_pass(const SortArgs& A, int nchunks, int w, hipStream_t s);
 hipError_t launch_build_rec(const SortArgs& A, int nchunks, hipStream_t s);
+// Instances of at most SORT_REC_MAX requests: keys, stable radix sort, records,
+// ranks and cleared outputs in one kernel, one workgroup per segment.
+enum { SORT_REC_MAX = 8192 };
+hipError_t prepare_sort_rec(int max_n);
+hipError_t launch_sort_rec(const SortArgs& A, int G, int max_n, hipStream_t s);
 hipError_t prepare_sim(bool d_lds, size_t lds_bytes);
 hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, size_t lds_bytes,
                       hipStream_t s);

@@ -238,6 +238,158 @@ __global__ __launch_bounds__(256) void k_build_rec(SortArgs A) {
     }
 }
 
+// One workgroup per segment whose instance holds n <= NT*E requests: the
+// priority keys (Eq. 1 / Eq. 2, SJF, FCFS), a stable least-significant-digit
+// radix sort on them (4-bit digits, as many passes as the policy's largest key
+// needs; requests start in index order, which is arrival order, so equal keys
+// stay in (arrival, index) order), then the rank-ordered records, the
+// index -> rank map and the cleared outputs.  Thread t holds the elements
+// t*E .. t*E+E-1 of the current order.  One pass: each element takes a
+// running count of its digit among the thread's earlier elements (a 16-bit
+// LDS counter per digit and thread, two to a 32-bit word for the atomic add),
+// an exclusive scan over the counters in digit-major order turns them into
+// start positions, and the elements are scattered through LDS and read back
+// in thread order.  The element array is padded by one entry per 32 so that
+// the thread-strided reads spread over the banks.  Global memory is read and
+// written in batches of 8 elements per thread, so that a thread has 8
+// requests in flight.
+__device__ __forceinline__ int pad32(int f) { return f + (f >> 5); }
+
+template <int NT, int E>
+__global__ __launch_bounds__(NT) void k_sort_rec(SortArgs A) {
+    constexpr int CH = NT * E;
+    constexpr int B8 = 8;
+    extern __shared__ uint64_t smem[];
+    uint64_t* buf = smem;                                                 // [pad32(CH)]
+    uint16_t* cnt = reinterpret_cast<uint16_t*>(smem + CH + CH / 32);     // [16 NT]
+    uint32_t* cnt32 = reinterpret_cast<uint32_t*>(cnt);
+    uint32_t* wsum = reinterpret_cast<uint32_t*>(cnt + 16 * NT);          // [NT / 64]
+    const int g = blockIdx.x;
+    const int pol = g / A.I, inst = g - pol * A.I;
+    const int64_t off = A.offsets[inst];
+    const int n = (int)(A.offsets[inst + 1] - off);
+    const int policy = A.policies[pol] & 0xFF;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, w = tid >> 6;
+    const int64_t base = (int64_t)pol * A.N + off;
+
+    // keys, read coalesced (element j = (e0 + u) NT + t) and handed over through LDS
+    for (int e0 = 0; e0 * NT < n; e0 += B8) {
+        int ra[B8], rs[B8], ro[B8];
+#pragma unroll
+        for (int u = 0; u < B8; ++u) {
+            const int j = (e0 + u) * NT + tid;
+            if (j < n) {
+                const int64_t i = off + j;
+                ra[u] = A.a[i];
+                rs[u] = A.s[i];
+                ro[u] = planned_len(policy, A.o, A.plan, A.bit, A.O0, A.O1, i);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < B8; ++u) {
+            const int j = (e0 + u) * NT + tid;
+            if (j < n) buf[pad32(j)] = (priority_key(policy, ra[u], rs[u], ro[u]) << 32) | (uint32_t)j;
+        }
+    }
+    __syncthreads();
+    uint64_t v[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int j = tid * E + e;
+        v[e] = j < n ? buf[pad32(j)] : ~0ull;
+    }
+    const int kb = A.kbits[pol];
+    for (int sh = 0; sh < kb; sh += 4) {
+#pragma unroll
+        for (int d = 0; d < 16; ++d) cnt[d * NT + tid] = 0;
+        int dg[E];
+        uint32_t rk[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            dg[e] = (int)((v[e] >> (32 + sh)) & 15u);
+            rk[e] = 0u;
+            if (tid * E + e < n) {
+                const int f = dg[e] * NT + tid;
+                const int hs = 16 * (f & 1);
+                rk[e] = (atomicAdd(&cnt32[f >> 1], 1u << hs) >> hs) & 0xFFFFu;
+            }
+        }
+        __syncthreads();
+        // exclusive scan of the counters in digit-major order: thread t takes
+        // the entries 16t .. 16t+15, then the threads' totals are scanned
+        uint32_t c[16];
+        uint32_t tot = 0u;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const uint32_t x = cnt[16 * tid + k];
+            c[k] = tot;
+            tot += x;
+        }
+        uint32_t inc = tot;  // inclusive scan of the thread totals inside the wave
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t y = (uint32_t)__shfl_up((int)inc, o);
+            if (lane >= o) inc += y;
+        }
+        if (lane == 63) wsum[w] = inc;
+        __syncthreads();
+        uint32_t woff = 0u;
+        for (int k = 0; k < w; ++k) woff += wsum[k];
+        const uint32_t add = woff + inc - tot;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) cnt[16 * tid + k] = (uint16_t)(c[k] + add);
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (tid * E + e < n) buf[pad32((int)(cnt[dg[e] * NT + tid] + rk[e]))] = v[e];
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (tid * E + e < n) v[e] = buf[pad32(tid * E + e)];
+        __syncthreads();
+    }
+    // (with no pass, buf already holds the index order)
+    // records in rank order (consecutive ranks across a wave), the index ->
+    // rank map, and the outputs cleared
+    int4* rec = A.rec + base;
+    int32_t* rank = A.rank + base;
+    for (int e0 = 0; e0 * NT < n; e0 += B8) {
+        int idx[B8];
+        int4 q[B8];
+#pragma unroll
+        for (int u = 0; u < B8; ++u) {
+            const int r = (e0 + u) * NT + tid;
+            idx[u] = r < n ? (int)(uint32_t)buf[pad32(r)] : -1;
+            if ((unsigned)idx[u] >= (unsigned)n) idx[u] = -1;  // only a broken sort
+        }
+#pragma unroll
+        for (int u = 0; u < B8; ++u) {
+            if (idx[u] >= 0) {
+                const int64_t i = off + idx[u];
+                q[u].x = idx[u];
+                q[u].y = A.s[i];
+                q[u].z = planned_len(policy, A.o, A.plan, A.bit, A.O0, A.O1, i);
+                q[u].w = A.o[i];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < B8; ++u) {
+            const int r = (e0 + u) * NT + tid;
+            if (idx[u] >= 0) {
+                rec[r] = q[u];
+                rank[idx[u]] = r;
+            }
+            if (r < n) {
+                A.start[base + r] = -1;
+                A.fin[base + r] = -1;
+                A.preempt[base + r] = 0;
+                A.admit_seq[base + r] = -1;
+            }
+        }
+    }
+}
+
 // ------------------------------------------------------------ simulation
 
 struct Seg {
@@ -1111,6 +1263,46 @@ hipError_t launch_build_rec(const SortArgs& A, int nchunks, hipStream_t s) {
     if (nchunks <= 0) return hipSuccess;
     hipLaunchKernelGGL(k_build_rec, dim3(nchunks), dim3(256), 0, s, A);
     return hipGetLastError();
+}
+
+template <int NT, int E>
+static size_t sort_rec_lds() {
+    return (size_t)(NT * E + NT * E / 32) * 8 + (size_t)16 * NT * 2 + (size_t)(NT / 64) * 4;
+}
+
+template <int NT, int E>
+static hipError_t sort_rec_attr() {
+    const size_t b = sort_rec_lds<NT, E>();
+    if (b <= 65536) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_sort_rec<NT, E>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)b);
+}
+
+template <int NT, int E>
+static hipError_t sort_rec_go(const SortArgs& A, int G, hipStream_t s) {
+    const size_t lds = sort_rec_lds<NT, E>();
+    hipLaunchKernelGGL((k_sort_rec<NT, E>), dim3(G), dim3(NT), lds, s, A);
+    return hipGetLastError();
+}
+
+// workgroup shapes (threads, elements per thread) by the largest instance
+hipError_t prepare_sort_rec(int max_n) {
+    if (max_n <= 64 * 4) return sort_rec_attr<64, 4>();
+    if (max_n <= 128 * 8) return sort_rec_attr<128, 8>();
+    if (max_n <= 128 * 16) return sort_rec_attr<128, 16>();
+    if (max_n <= 256 * 16) return sort_rec_attr<256, 16>();
+    if (max_n <= 256 * 32) return sort_rec_attr<256, 32>();
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_sort_rec(const SortArgs& A, int G, int max_n, hipStream_t s) {
+    if (G <= 0) return hipSuccess;
+    if (max_n <= 64 * 4) return sort_rec_go<64, 4>(A, G, s);
+    if (max_n <= 128 * 8) return sort_rec_go<128, 8>(A, G, s);
+    if (max_n <= 128 * 16) return sort_rec_go<128, 16>(A, G, s);
+    if (max_n <= 256 * 16) return sort_rec_go<256, 16>(A, G, s);
+    if (max_n <= 256 * 32) return sort_rec_go<256, 32>(A, G, s);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, size_t lds_bytes,

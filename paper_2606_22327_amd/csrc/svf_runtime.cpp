@@ -60,6 +60,8 @@ struct svf_batch {
     std::vector<int32_t> policies;
     std::vector<int64_t> offsets;
     int32_t H = 1, CH = 64, nchunks = 0, bw_max = 0, max_n = 0;
+    bool fused_sort = false;  // every instance fits one workgroup of k_sort_rec
+    int32_t kbits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t bw_total = 0;
     bool d_lds = true;
     size_t lds_bytes = 0;
@@ -142,7 +144,8 @@ struct HostView {
 
 // Everything that can be checked without a GPU.
 int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64_t>& off,
-             int64_t N, std::vector<uint8_t>* stepped, int64_t* max_plan, int64_t* max_profile) {
+             int64_t N, std::vector<uint8_t>* stepped, int64_t* max_plan, int64_t* max_profile,
+             std::vector<uint64_t>* max_key) {
     const int32_t I = d->num_instances, P = d->num_policies;
     bool has1bit = false;
     for (int p = 0; p < P; ++p) has1bit |= (d->policies[p] & 0xFF) == SVF_POLICY_SVF1BIT;
@@ -156,6 +159,7 @@ int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64
     // instance bound it together: sum of s + o^.
     *max_profile = d->M;
     stepped->assign((size_t)P * I, 0);
+    max_key->assign(P, 0);
     std::vector<int64_t> cur_total(P);
     for (int32_t i = 0; i < I; ++i) {
         const int64_t lo = off[i], hi = off[i + 1];
@@ -192,6 +196,7 @@ int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64
                 if (key >= (uint64_t(1) << 32))
                     return fail(SVF_EINVAL, "instance %d request %lld: priority key %llu >= 2^32", i,
                                 (long long)(j - lo), (unsigned long long)key);
+                (*max_key)[p] = std::max((*max_key)[p], key);
                 // eviction is only possible when plans differ from the truth
                 // or when admission looks at the next step only
                 if (oh != o || current_rule) (*stepped)[(size_t)p * I + i] = 1;
@@ -257,10 +262,12 @@ int do_reset(svf_batch* h) {
     HIPCHK(svfk::launch_init_state(h->d_st, G, h->stream));
     HIPCHK(svfk::launch_fill_u64(h->d_bitmap, (int64_t)h->P * h->bw_total, 0ull, h->stream));
     HIPCHK(svfk::launch_init_ring(h->d_ring, (int64_t)G * (h->H + 64), h->H, h->stream));
-    HIPCHK(svfk::launch_fill_i32(h->d_start, PN, -1, h->stream));
-    HIPCHK(svfk::launch_fill_i32(h->d_fin, PN, -1, h->stream));
-    HIPCHK(svfk::launch_fill_i32(h->d_pre, PN, 0, h->stream));
-    HIPCHK(svfk::launch_fill_i32(h->d_seq, PN, -1, h->stream));
+    if (!h->fused_sort) {
+        HIPCHK(svfk::launch_fill_i32(h->d_start, PN, -1, h->stream));
+        HIPCHK(svfk::launch_fill_i32(h->d_fin, PN, -1, h->stream));
+        HIPCHK(svfk::launch_fill_i32(h->d_pre, PN, 0, h->stream));
+        HIPCHK(svfk::launch_fill_i32(h->d_seq, PN, -1, h->stream));
+    }
     if (PN > 0) {
         svfk::SortArgs A{};
         A.offsets = h->d_off;
@@ -271,6 +278,16 @@ int do_reset(svf_batch* h) {
         A.rec = h->d_rec;
         A.rank = h->d_rank;
         A.I = h->I; A.P = h->P; A.N = h->N; A.O0 = h->O0; A.O1 = h->O1; A.CH = h->CH;
+        for (int p = 0; p < 8; ++p) A.kbits[p] = h->kbits[p];
+        A.start = h->d_start; A.fin = h->d_fin; A.preempt = h->d_pre; A.admit_seq = h->d_seq;
+        if (h->fused_sort) {
+            // keys, sort, records, ranks and cleared outputs in one kernel
+            HIPCHK(svfk::launch_sort_rec(A, G, h->max_n, h->stream));
+            record_end(h, 0, e0);
+            h->was_reset = true;
+            h->dirty = true;
+            return SVF_OK;
+        }
         A.keys_in = nullptr;
         A.keys_out = h->d_keys0;
         HIPCHK(svfk::launch_chunk_sort(A, h->nchunks, h->stream));
@@ -396,7 +413,8 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     }
     std::vector<uint8_t> stepped;
     int64_t max_plan = 1, max_profile = 0;
-    RETCHK(validate(d, v, off, N, &stepped, &max_plan, &max_profile));
+    std::vector<uint64_t> max_key;
+    RETCHK(validate(d, v, off, N, &stepped, &max_plan, &max_profile, &max_key));
 
     svf_batch* h = new (std::nothrow) svf_batch();
     if (!h) return fail(SVF_ENOMEM, "host allocation failed");
@@ -411,6 +429,9 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     h->H = (int32_t)next_pow2(std::max<int64_t>(max_plan, 1));
     for (int32_t i = 0; i < I; ++i) h->max_n = std::max<int32_t>(h->max_n, (int32_t)(off[i + 1] - off[i]));
     h->CH = (int32_t)std::min<int64_t>(8192, std::max<int64_t>(64, next_pow2(h->max_n)));
+    h->fused_sort = h->max_n <= svfk::SORT_REC_MAX;
+    for (int32_t p = 0; p < P; ++p)
+        h->kbits[p] = max_key[p] ? 64 - __builtin_clzll(max_key[p]) : 0;
     for (uint8_t x : stepped) {
         h->any_stepped |= x != 0;
         (x ? h->n_stepped : h->n_known) += 1;
@@ -470,8 +491,10 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     ALLOC(d_pol, P);
     ALLOC(d_chunk_seg, h->nchunks);
     ALLOC(d_chunk_lo, h->nchunks);
-    ALLOC(d_keys0, PN);
-    ALLOC(d_keys1, PN);
+    if (!h->fused_sort) {
+        ALLOC(d_keys0, PN);
+        ALLOC(d_keys1, PN);
+    }
     ALLOC(d_rec, PN);
     ALLOC(d_rank, PN);
     ALLOC(d_stepped, G);
@@ -514,6 +537,10 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess) {
         hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes);
+        if (a != hipSuccess) e = a;
+    }
+    if (e == hipSuccess && h->fused_sort) {
+        hipError_t a = svfk::prepare_sort_rec(h->max_n);
         if (a != hipSuccess) e = a;
     }
     if (e != hipSuccess) {

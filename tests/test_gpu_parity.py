@@ -235,6 +235,42 @@ def test_ragged_sizes_with_merge_passes():
         compare(b, g[pol], pol, label="ragged")
 
 
+def test_fused_sort_shapes_boundary_and_wide_keys():
+    """Instances sorted by the one-workgroup radix sort in each of its
+    workgroup shapes (largest instance 200, 1000, 2000, 4000 and exactly 8192
+    requests), the first size past it (8193, sorted in chunks and merged),
+    and SVF keys just below 2^32 (eight radix passes) next to tiny ones."""
+    rng = np.random.default_rng(2606)
+
+    def part(n, s_hi, o_hi, gap):
+        a = np.floor(np.cumsum(rng.exponential(gap, n))).astype(np.int64)
+        return {"arrival": a, "prompt": rng.integers(1, s_hi + 1, n),
+                "output": rng.integers(1, o_hi + 1, n)}
+
+    for top in (200, 1000, 2000, 4000, 8192, 8193):
+        sizes = [top, 0, 1, max(1, top // 3), 7]
+        parts = [part(n, 300, 400, 0.3) for n in sizes]
+        b = W.assemble(f"shape{top}", parts, 4096, ("svf", "sjf", "fcfs"))
+        say(f"fused sort shape, largest instance {top}")
+        g = gpu_run(b)
+        for pol in b.policies:
+            compare(b, g[pol], pol, label=f"shape{top}")
+    # s * o + o(o+1)/2 up to 53000 * 53000 + 53000 * 53001 / 2 < 2^32
+    wide = []
+    for n in (300, 40):
+        p = part(n, 10, 10, 2.0)
+        k = rng.random(n) < 0.3
+        p["prompt"] = np.where(k, rng.integers(45000, 53001, n), p["prompt"])
+        p["output"] = np.where(k, rng.integers(45000, 53001, n), p["output"])
+        wide.append(p)
+    b = W.assemble("widekeys", wide, 140000, ("svf",))
+    key = b.prompt.astype(np.int64) * b.output + (b.output.astype(np.int64) ** 2 + b.output) // 2
+    assert int(key.max()).bit_length() == 32
+    say("keys just below 2^32")
+    g = gpu_run(b)
+    compare(b, g["svf"], "svf", label="widekeys")
+
+
 def test_degenerate_cases():
     say("degenerate cases")
     # all instances empty
