@@ -79,7 +79,8 @@ struct SimArgs {
     int32_t* fin;
     int32_t* preempt;
     int32_t* admit_seq;
-    int32_t* act;             // [P*N] or null
+    int4* act;                // [P*N] or null: running list, record of each entry
+    int2* actkr;              // [P*N] or null: running list, {start step, rank}
     int32_t* evl;             // [P*N] or null
     SegState* st;             // [G]
     int32_t I, P;

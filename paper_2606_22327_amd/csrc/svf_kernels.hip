@@ -401,7 +401,8 @@ struct Seg {
     int32_t* __restrict__ fin;
     int32_t* __restrict__ preempt;
     int32_t* __restrict__ admit_seq;
-    int32_t* __restrict__ act;
+    int4* __restrict__ act;      // running list (per-step path): record {index, s, o^, o}
+    int2* __restrict__ actkr;    //   and {start step, rank}
     int32_t* __restrict__ evl;
 };
 
@@ -936,86 +937,157 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
 
 // ---- planned lengths differ from the truth: one step at a time
 
+// The running list (global memory, small enough to stay in L2): entry x
+// holds the record {index, s, planned length, true length} of a running
+// request and {start step, rank}.
+struct RunList {
+    int4* q;
+    int2* kr;
+    // entries written by one lane are read by others next
+    __device__ __forceinline__ static void order() { __syncthreads(); }
+};
+
 template <bool LDS>
 __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
-                            const Ring<LDS>& D, SegState& st, int t_lim) {
+                            const Ring<LDS>& D, const RunList& A, SegState& st, int t_lim) {
     const int lane = lane_id();
     const int M = P.M;
-    int t = st.t, cursor = st.cursor, seq = st.seq, nfin = st.nfin, nA = st.nA, N_O = st.N_O;
+    const int n = sg.n;
+    int t = uni(st.t), cursor = uni(st.cursor), seq = uni(st.seq), nfin = uni(st.nfin);
+    int nA = uni(st.nA), N_O = uni(st.N_O);
     int64_t C_O = st.C_O, peak = st.peak, req_steps = st.req_steps;
     int status = STATUS_RUNNING;
     // no request admitted so far is planned to hold memory after step maxF
-    int maxF = st.max_fin;
+    int maxF = uni(st.max_fin);
     // current-capacity admission checks the next step only
     const int pol = blockIdx.x / P.I;
     const int chk = (P.policies[pol] & ADMIT_CURRENT) ? 1 : (1 << 30);
     // memory planned for step t+1 by requests within their planned length
     auto planned_next = [&]() -> int64_t { return (int64_t)D.ld(t + 1) - (t + 1); };
+
+    // arrival window: lane l holds the arrival and rank of request wb + l
+    int wb = 0, a_reg = INT32_MAX, rk_reg = 0;
+    auto load_arrivals = [&](int b) {
+        wb = uni(b);
+        const int i = b + lane;
+        a_reg = INT32_MAX;
+        rk_reg = 0;
+        if (i < n) {
+            a_reg = sg.a[i];
+            rk_reg = sg.rank[i];
+            if ((unsigned)rk_reg >= (unsigned)n) rk_reg = 0;  // only a broken sort
+        }
+    };
+    load_arrivals(cursor);
+    // rank window: lane l holds the record of rank rwb + l
+    int rwb = INT32_MIN / 2;
+    int4 rw = make_int4(0, 0, 0, 0);
+    auto rec_of = [&](int r) -> int4 {
+        if (r < rwb || r >= rwb + 64) {
+            rwb = uni(r & ~63);
+            rw = sg.rec[min(rwb + lane, n - 1)];
+        }
+        return readlane4(rw, r - rwb);
+    };
+    // Steps that provably change nothing are not scanned or checked:
+    //  - next_ev: no running request completes or reaches its planned length
+    //    before this step (the list is scanned only from then on);
+    //  - blk, blk_tf: the highest-priority waiting request (rank blk) failed
+    //    the check and cannot fit before step blk_tf while the planned
+    //    profile has not shrunk and no request of higher priority is waiting
+    //    (relaxed is set by completions, evictions and such arrivals).
+    //    A violation at a future step tau persists until tau or until
+    //    G[tau] - (M - s) is reached; one at the next step persists until
+    //    something is released, since the true memory of the next step only
+    //    grows while no request completes or leaves.
+    int next_ev = t;  // scan at the first step of a launch
+    int blk = -1, blk_tf = 0;
+    bool relaxed = true;
+
     for (;;) {
-        if (nfin == sg.n) { status = STATUS_DONE; break; }
+        if (nfin == n) { status = STATUS_DONE; break; }
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
         if (t >= t_lim) break;
-        // 1. arrivals
-        while (cursor < sg.n) {
-            const int i = cursor + lane;
-            const bool arr = (i < sg.n) && (sg.a[i] == t);
+        // 1. arrivals: a prefix of the window (arrivals are sorted)
+        for (;;) {
+            const bool arr = (wb + lane >= cursor) && (a_reg == t);
             const uint64_t m = ballot(arr);
             if (m == 0ull) break;
-            if (arr) {
-                const int r = sg.rank[i];
-                if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
-            }
-            const int cnt = __popcll(m);
-            cursor += cnt;
-            if (cnt < 64) break;
+            if (arr) bitmap_set_atomic(B, S, rk_reg);
+            if (ballot(arr && (blk < 0 || rk_reg < blk)) != 0ull) relaxed = true;
+            cursor += __popcll(m);
+            if (cursor < wb + 64) break;
+            load_arrivals(cursor);
         }
         lds_order();
-        // 2. completions and requests reaching their planned length
-        {
+        // 2. completions and requests reaching their planned length: a group
+        //    of up to 256 entries is read at once, then compacted in place
+        //    (kept entries only move to lower slots)
+        if (nA > 0 && t >= next_ev) {
             int newA = 0;
             int64_t dC = 0;
             int dN = 0, dfin = 0;
-            for (int base = 0; base < nA; base += 64) {
-                const int x = base + lane;
-                int r = -1, idx = 0, s = 0, oh = 0, o = 0, k = 0;
-                bool live = x < nA, done = false;
-                if (live) {
-                    r = sg.act[x];
-                    const int4 q = sg.rec[r];
-                    idx = q.x; s = q.y; oh = q.z; o = q.w;
-                    k = sg.start[idx];
-                    const int e = t - k;
-                    if (e == o) {
-                        done = true;
-                        sg.fin[idx] = t;
-                        if (o > oh) { dC -= (int64_t)(s - k); dN -= 1; }
-                    } else if (e == oh) {
-                        dC += (int64_t)(s - k);
-                        dN += 1;
+            int nxt = INT32_MAX;  // next event of the entries that stay
+            for (int base = 0; base < nA; base += 256) {
+                int4 qq[4];
+                int2 kr[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int x = min(base + 64 * u + lane, nA - 1);
+                    qq[u] = A.q[x];
+                    kr[u] = A.kr[x];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int x = base + 64 * u + lane;
+                    const bool live = x < nA;
+                    const int idx = qq[u].x, s = qq[u].y, oh = qq[u].z, o = qq[u].w, k = kr[u].x;
+                    bool done = false;
+                    if (live) {
+                        const int e = t - k;
+                        if (e == o) {
+                            done = true;
+                            sg.fin[idx] = t;
+                            if (o > oh) { dC -= (int64_t)(s - k); dN -= 1; }
+                        } else if (e == oh) {
+                            dC += (int64_t)(s - k);
+                            dN += 1;
+                        }
+                        if (!done) nxt = min(nxt, (e < oh && oh < o) ? k + oh : k + o);
                     }
+                    const uint64_t dm = ballot(done);
+                    if (dm == 0ull) {  // nothing leaves: entries stay (or move down)
+                        const int pos = newA + lane;
+                        if (live && pos != x) { A.q[pos] = qq[u]; A.kr[pos] = kr[u]; }
+                        newA += __popcll(ballot(live));
+                        continue;
+                    }
+                    // early finishers give back their planned future
+                    uint64_t early = ballot(done && oh > o);
+                    while (early) {
+                        const int src = __builtin_ctzll(early);
+                        early &= early - 1;
+                        remove_future(D, t, __builtin_amdgcn_readlane(s, src),
+                                      __builtin_amdgcn_readlane(k, src),
+                                      __builtin_amdgcn_readlane(oh, src));
+                    }
+                    const uint64_t keep = ballot(live && !done);
+                    dfin += __popcll(dm);
+                    const int pos = newA + __popcll(keep & ((1ull << lane) - 1ull));
+                    if (live && !done) {
+                        A.q[pos] = qq[u];
+                        A.kr[pos] = kr[u];
+                    }
+                    newA += __popcll(keep);
                 }
-                // early finishers give back their planned future
-                uint64_t early = ballot(done && oh > o);
-                while (early) {
-                    const int src = __builtin_ctzll(early);
-                    early &= early - 1;
-                    remove_future(D, t, __builtin_amdgcn_readlane(s, src),
-                                  __builtin_amdgcn_readlane(k, src),
-                                  __builtin_amdgcn_readlane(oh, src));
-                }
-                const uint64_t keep = ballot(live && !done);
-                dfin += __popcll(ballot(done));
-                // in-place compaction: every kept entry moves to a lower or equal slot
-                const int pos = newA + __popcll(keep & ((1ull << lane) - 1ull));
-                __syncthreads();
-                if (live && !done) sg.act[pos] = r;
-                newA += __popcll(keep);
-                __syncthreads();
             }
-            nA = newA;
+            nA = uni(newA);
             C_O += wave_sum_i64(dC);
             N_O += (int)wave_sum_i64(dN);
+            if (dfin > 0) relaxed = true;
             nfin += dfin;
+            next_ev = wmin(nxt);
+            RunList::order();  // the compacted list is read again below
         }
         // 3. overflow of the true memory at t+1: evict the largest believed
         //    remaining volume (latest arrival on ties)
@@ -1025,65 +1097,98 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             while (mem_next > M && nA > 0) {
                 long long bestR = -1;
                 int bestIdx = -1, bestPos = -1;
-                for (int x = lane; x < nA; x += 64) {
-                    const int4 q = sg.rec[sg.act[x]];
-                    const int k = sg.start[q.x];
-                    const long long e = t - k;
-                    const long long L = max((long long)q.z, e + 1);
-                    const long long R = (L - e) * q.y + (L * (L + 1) - e * (e + 1)) / 2;
-                    if (R > bestR || (R == bestR && q.x > bestIdx)) { bestR = R; bestIdx = q.x; bestPos = x; }
+                for (int base = 0; base < nA; base += 256) {
+                    int4 qq[4];
+                    int2 kr[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int x = min(base + 64 * u + lane, nA - 1);
+                        qq[u] = A.q[x];
+                        kr[u] = A.kr[x];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int x = base + 64 * u + lane;
+                        if (x >= nA) continue;
+                        const long long e = t - kr[u].x;
+                        const long long L = max((long long)qq[u].z, e + 1);
+                        const long long R = (L - e) * qq[u].y + (L * (L + 1) - e * (e + 1)) / 2;
+                        if (R > bestR || (R == bestR && qq[u].x > bestIdx)) {
+                            bestR = R;
+                            bestIdx = qq[u].x;
+                            bestPos = x;
+                        }
+                    }
                 }
                 const long long gR = wave_max_i64(bestR);
                 const int gIdx = wmax(bestR == gR ? bestIdx : -1);
                 const uint64_t who = ballot(bestR == gR && bestIdx == gIdx);
                 const int src = __builtin_ctzll(who);
                 const int vpos = __builtin_amdgcn_readlane(bestPos, src);
-                const int vr = sg.act[vpos];
-                const int4 q = sg.rec[vr];
-                const int k = sg.start[q.x];
+                const int4 q = A.q[vpos];
+                const int2 vkr = A.kr[vpos];
+                const int k = vkr.x;
                 const int e = t - k;
                 if (e < q.z) remove_future(D, t, q.y, k, q.z);
                 else { C_O -= (int64_t)(q.y - k); N_O -= 1; }
-                __syncthreads();
                 if (lane == 0) {
-                    sg.act[vpos] = sg.act[nA - 1];
+                    A.q[vpos] = A.q[nA - 1];
+                    A.kr[vpos] = A.kr[nA - 1];
                     sg.preempt[q.x] += 1;
                     sg.start[q.x] = -1;
                     sg.admit_seq[q.x] = -1;
-                    sg.evl[nev] = vr;
+                    sg.evl[nev] = vkr.y;
                 }
-                __syncthreads();
+                RunList::order();
                 --nA;
                 ++nev;
+                relaxed = true;
                 mem_next = planned_next() + C_O + (int64_t)N_O * (t + 1);
             }
         }
         // 4. admissions
         for (;;) {
+            if (!relaxed && blk >= 0 && t < blk_tf) break;  // still blocked
             const int r = bitmap_first(B, S, W1);
-            if (r < 0) break;
-            const int4 q = sg.rec[r];
+            if (r < 0) { blk = -1; break; }
+            const int4 q = rec_of(r);
             int tf = 0;
             // memory of requests past their plan at t+1; <= M after step 3
             const int extra1 = (int)(C_O + (int64_t)N_O * (t + 1));
-            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, maxF, &tf, chk)) break;
+            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, maxF, &tf, chk)) {
+                blk = r;
+                // If the next step alone is over (true memory at t+1 plus the
+                // candidate's first token), the candidate stays blocked until
+                // something is released: without completions or evictions the
+                // running set only grows, by one token per request per step.
+                const bool over1 = planned_next() + extra1 + q.y + 1 > M;
+                blk_tf = over1 ? INT32_MAX : tf;
+                relaxed = false;
+                break;
+            }
             maxF = max(maxF, t + q.z);
+            next_ev = min(next_ev, q.z < q.w ? t + q.z : t + q.w);
             if (lane == 0) {
                 bitmap_clear(B, S, r);
                 sg.start[q.x] = t;
                 sg.admit_seq[q.x] = seq;
-                sg.act[nA] = r;
+                A.q[nA] = q;
+                A.kr[nA] = make_int2(t, r);
             }
-            __syncthreads();
+            RunList::order();
             ++seq;
             ++nA;
         }
         // evicted requests compete again from the next step
-        for (int x = lane; x < nev; x += 64) {
-            const int r = sg.evl[x];
-            if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
+        if (nev > 0) {
+            __syncthreads();  // their ranks were stored by lane 0
+            for (int x = lane; x < nev; x += 64) {
+                const int r = sg.evl[x];
+                if ((unsigned)r < (unsigned)n) bitmap_set_atomic(B, S, r);
+            }
+            lds_order();
+            relaxed = true;  // one of them may rank above the blocked head
         }
-        __syncthreads();
         // 5. advance
         req_steps += nA;
         const int64_t mem = planned_next() + C_O + (int64_t)N_O * (t + 1);
@@ -1124,6 +1229,7 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     sg.preempt = P.preempt + base;
     sg.admit_seq = P.admit_seq + base;
     sg.act = P.act ? P.act + base : nullptr;
+    sg.actkr = P.actkr ? P.actkr + base : nullptr;
     sg.evl = P.evl ? P.evl + base : nullptr;
 
     // rank bitmap (two levels) staged in LDS for the launch
@@ -1151,8 +1257,14 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     D.p = D_LDS ? Dl : Dg;
     D.H = P.H;
     D.mask = P.H - 1;
-    if (STEPPED) run_stepped(P, sg, B, S, W1, D, st, t_lim);
-    else run_known(P, sg, B, S, W1, D, st, t_lim);
+    if (STEPPED) {
+        RunList L;
+        L.q = sg.act;
+        L.kr = sg.actkr;
+        run_stepped(P, sg, B, S, W1, D, L, st, t_lim);
+    } else {
+        run_known(P, sg, B, S, W1, D, st, t_lim);
+    }
     __syncthreads();
     for (int x = lane; x < W0 + W1; x += 64) Bg[x] = B[x];
     if (D_LDS) {

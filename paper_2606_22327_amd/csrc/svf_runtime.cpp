@@ -87,7 +87,9 @@ struct svf_batch {
     uint64_t* d_bitmap = nullptr;
     int32_t* d_ring = nullptr;
     int32_t *d_start = nullptr, *d_fin = nullptr, *d_pre = nullptr, *d_seq = nullptr;
-    int32_t *d_act = nullptr, *d_evl = nullptr;
+    int4* d_act = nullptr;
+    int2* d_actkr = nullptr;
+    int32_t* d_evl = nullptr;
     SegState* d_st = nullptr;
     int32_t* d_fin_out = nullptr;
     StatsOut* d_stats = nullptr;
@@ -113,7 +115,7 @@ void free_all(svf_batch* h) {
     void* ptrs[] = {h->d_off, h->d_a, h->d_s, h->d_o, h->d_plan, h->d_bit, h->d_pol,
                     h->d_chunk_seg, h->d_chunk_lo, h->d_keys0, h->d_keys1, h->d_rec,
                     h->d_rank, h->d_stepped, h->d_bw_off, h->d_bitmap, h->d_ring,
-                    h->d_start, h->d_fin, h->d_pre, h->d_seq, h->d_act, h->d_evl,
+                    h->d_start, h->d_fin, h->d_pre, h->d_seq, h->d_act, h->d_actkr, h->d_evl,
                     h->d_st, h->d_fin_out, h->d_stats};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
@@ -327,6 +329,7 @@ int do_sim(svf_batch* h, int64_t delta) {
     S.preempt = h->d_pre;
     S.admit_seq = h->d_seq;
     S.act = h->d_act;
+    S.actkr = h->d_actkr;
     S.evl = h->d_evl;
     S.st = h->d_st;
     S.I = h->I; S.P = h->P; S.N = h->N;
@@ -507,6 +510,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     ALLOC(d_seq, PN);
     if (h->any_stepped) {
         ALLOC(d_act, PN);
+        ALLOC(d_actkr, PN);
         ALLOC(d_evl, PN);
     }
     ALLOC(d_st, G);

@@ -271,6 +271,22 @@ def test_fused_sort_shapes_boundary_and_wide_keys():
     compare(b, g["svf"], "svf", label="widekeys")
 
 
+def test_stepped_many_concurrent_tiny_prompts():
+    """The per-step path with more than a thousand requests running at once
+    (tiny prompts), next-step admission and evictions, against the oracle."""
+    rng = np.random.default_rng(77)
+    parts = []
+    for n in (1500, 300, 2):
+        a = np.floor(np.cumsum(rng.exponential(0.05, n))).astype(np.int64)
+        parts.append({"arrival": a, "prompt": rng.integers(1, 3, n),
+                      "output": rng.integers(1, 40, n)})
+    b = W.assemble("tinyprompts", parts, 3000, ("svf+cur", "sjf+cur"))
+    say("stepped: 1500 tiny prompts, M = 3000, next-step admission")
+    g = gpu_run(b)
+    for pol in b.policies:
+        compare(b, g[pol], pol, label="tinyprompts")
+
+
 def test_degenerate_cases():
     say("degenerate cases")
     # all instances empty
