@@ -564,30 +564,77 @@ __device__ __forceinline__ int window_max(const Ring<LDS>& R, int t, int len) {
     return m;
 }
 
+// Scan of the window [t+1, t+len] in batches of 64*NB slots (NB loads per
+// lane in flight): MODE 0 takes the largest G, MODE 1 the largest
+// min(tau, G - X), MODE 2 both.
+template <int NB, int MODE, bool LDS>
+__device__ __forceinline__ void window_scan(const Ring<LDS>& R, int t, int len, int X, int& m,
+                                            int& rel) {
+    const int lane = lane_id();
+    R.runs(t, len, [&](int s, int L, int tau0) {
+        const int32_t* q = R.p + s + lane;
+        int tau = tau0 + lane;
+        int b = 0;
+        for (; b + 64 * NB <= L; b += 64 * NB, q += 64 * NB, tau += 64 * NB) {
+            int x[NB];
+#pragma unroll
+            for (int u = 0; u < NB; ++u) x[u] = q[64 * u];
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                if (MODE != 1) m = max(m, x[u]);
+                if (MODE != 0) rel = max(rel, min(tau + 64 * u, x[u] - X));
+            }
+        }
+        for (; b + 256 <= L; b += 256, q += 256, tau += 256) {
+            int x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) x[u] = q[64 * u];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (MODE != 1) m = max(m, x[u]);
+                if (MODE != 0) rel = max(rel, min(tau + 64 * u, x[u] - X));
+            }
+        }
+        const int rem = uni(L - b);
+        if (rem > 0) {
+            const int base = s + b + lane;
+            int x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) x[u] = R.p[min(base + 64 * u, R.H - 1)];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool in = lane + 64 * u < rem;
+                if (MODE != 1) m = max(m, in ? x[u] : INT32_MIN);
+                if (MODE != 0) rel = max(rel, in ? min(tau + 64 * u, x[u] - X) : INT32_MIN);
+            }
+        }
+    });
+}
+
 // Add c0 + SLOPE * tau (SLOPE = +1 or -1) to every slot of the window
-// [t+1, t+len].
-template <int SLOPE, bool LDS>
-__device__ __forceinline__ void window_add_linear(const Ring<LDS>& R, int t, int len, int c0) {
+// [t+1, t+len] (len <= H), in batches of 64*NB slots, then 256, then a tail
+// with clamped loads and masked-off stores to the spare slot.
+template <int NB, int SLOPE, bool LDS>
+__device__ __forceinline__ void window_add(const Ring<LDS>& R, int t, int len, int c0) {
     const int lane = lane_id();
     R.runs(t, len, [&](int s, int L, int tau0) {
         int32_t* q = R.p + s + lane;
         int c = c0 + SLOPE * (tau0 + lane);
         int b = 0;
-        for (; b + 1024 <= L; b += 1024, q += 1024, c += SLOPE * 1024) {
-            int x[16];
+        for (; b + 64 * NB <= L; b += 64 * NB, q += 64 * NB, c += SLOPE * 64 * NB) {
+            int x[NB];
 #pragma unroll
-            for (int u = 0; u < 16; ++u) x[u] = q[64 * u];
+            for (int u = 0; u < NB; ++u) x[u] = q[64 * u];
 #pragma unroll
-            for (int u = 0; u < 16; ++u) q[64 * u] = x[u] + c + SLOPE * 64 * u;
+            for (int u = 0; u < NB; ++u) q[64 * u] = x[u] + c + SLOPE * 64 * u;
         }
         for (; b + 256 <= L; b += 256, q += 256, c += SLOPE * 256) {
-            const int x0 = q[0], x1 = q[64], x2 = q[128], x3 = q[192];
-            q[0] = x0 + c;
-            q[64] = x1 + c + SLOPE * 64;
-            q[128] = x2 + c + SLOPE * 128;
-            q[192] = x3 + c + SLOPE * 192;
+            int x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) x[u] = q[64 * u];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) q[64 * u] = x[u] + c + SLOPE * 64 * u;
         }
-        // tail: up to 255 slots, clamped loads, masked-off stores to the spare slot
         const int rem = uni(L - b);
         if (rem > 0) {
             const int base = s + b + lane;
@@ -611,7 +658,7 @@ __device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, in
                                           int live, int X, int lim, int extra1, int* t_free) {
     const int lane = lane_id();
     int g[U];
-    int m = INT32_MIN, rel = INT32_MIN;
+    int m = INT32_MIN;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int j = lane + 64 * u;
@@ -622,13 +669,18 @@ __device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, in
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int j = lane + 64 * u;
-        const int tau = t + 1 + j;
         const int v = g[u] + (j == 0 ? extra1 : 0);
-        const bool in = j < len;
-        m = max(m, in ? v : INT32_MIN);
-        rel = max(rel, in ? min(tau, v - X) : INT32_MIN);
+        m = max(m, j < len ? v : INT32_MIN);
     }
     if (ballot(m > lim) != 0ull) {
+        // the release step, from the values still in registers
+        int rel = INT32_MIN;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int j = lane + 64 * u;
+            const int v = g[u] + (j == 0 ? extra1 : 0);
+            rel = max(rel, j < len ? min(t + 1 + j, v - X) : INT32_MIN);
+        }
         *t_free = wmax(rel);
         return false;
     }
@@ -659,7 +711,6 @@ __device__ __forceinline__ bool fit_small(const Ring<LDS>& R, int t, int s_h, in
 template <bool LDS>
 __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h, int oh, int M,
                                               int extra1, int maxF, int* t_free, int chk = 1 << 30) {
-    const int lane = lane_id();
     const int X = M - s_h;
     const int lim = X + t;
     // steps of the candidate's window that hold planned memory, and the part checked
@@ -672,49 +723,18 @@ __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h
     if (oh <= 128) return fit_small<2>(R, t, s_h, oh, len, ld, X, lim, extra1, t_free);
     if (oh <= 256) return fit_small<4>(R, t, s_h, oh, len, ld, X, lim, extra1, t_free);
     if (oh <= 512) return fit_small<8>(R, t, s_h, oh, len, ld, X, lim, extra1, t_free);
+    // longer windows: the check takes only the maximum; the release step is
+    // computed in a second pass when the candidate does not fit
     int m = INT32_MIN, rel = INT32_MIN;
-    R.runs(t, len, [&](int s, int L, int tau0) {
-        const int32_t* q = R.p + s + lane;
-        int tau = tau0 + lane;
-        int b = 0;
-        for (; b + 1024 <= L; b += 1024, q += 1024, tau += 1024) {
-            int x[16];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) x[u] = q[64 * u];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) {
-                m = max(m, x[u]);
-                rel = max(rel, min(tau + 64 * u, x[u] - X));
-            }
-        }
-        for (; b + 256 <= L; b += 256, q += 256, tau += 256) {
-            const int x0 = q[0], x1 = q[64], x2 = q[128], x3 = q[192];
-            m = max(m, max(max(x0, x1), max(x2, x3)));
-            rel = max(rel, max(max(min(tau, x0 - X), min(tau + 64, x1 - X)),
-                               max(min(tau + 128, x2 - X), min(tau + 192, x3 - X))));
-        }
-        const int rem = uni(L - b);
-        if (rem > 0) {
-            const int base = s + b + lane;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int x = R.p[min(base + 64 * u, R.H - 1)];
-                const bool in = lane + 64 * u < rem;
-                m = max(m, in ? x : INT32_MIN);
-                rel = max(rel, in ? min(tau + 64 * u, x - X) : INT32_MIN);
-            }
-        }
-    });
-    if (extra1 != 0) {
-        const int v = R.ld(t + 1) + extra1;
-        m = max(m, v);
-        rel = max(rel, min(t + 1, v - X));
-    }
+    window_scan<16, 0>(R, t, len, X, m, rel);
+    if (extra1 != 0) m = max(m, R.ld(t + 1) + extra1);
     if (ballot(m > lim) != 0ull) {
+        window_scan<16, 1>(R, t, len, X, m, rel);
+        if (extra1 != 0) rel = max(rel, min(t + 1, R.ld(t + 1) + extra1 - X));
         *t_free = wmax(rel);
         return false;
     }
-    window_add_linear<1>(R, t, oh, s_h - t);
+    window_add<16, 1>(R, t, oh, s_h - t);
     return true;
 }
 
@@ -722,7 +742,7 @@ __device__ __forceinline__ bool fit_and_admit(const Ring<LDS>& R, int t, int s_h
 // for the future steps tau in [t+1, k+L].
 template <bool LDS>
 __device__ __forceinline__ void remove_future(const Ring<LDS>& R, int t, int s, int k, int L) {
-    window_add_linear<-1>(R, t, k + L - t, k - s);
+    window_add<16, -1>(R, t, k + L - t, k - s);
 }
 
 // Fold the past steps (lo, hi] (hi <= t): their memory is final; add it to
