@@ -26,7 +26,8 @@ struct SegState {
     int64_t C_O;        // per-step path: sum of (s - k) over those requests
     int64_t peak;       // largest memory total over the steps folded so far
     int64_t req_steps;  // per-step path: sum over steps of running requests
-    int64_t pad;
+    int32_t ln;         // event path with the list profile: running requests
+    uint32_t lq;        //   and the prefix sum of (s - k) of the last entry
 };
 
 // Same layout as svf_instance_stats of the public header.
@@ -91,6 +92,9 @@ struct SimArgs {
     int32_t M;
     int32_t max_steps;
     int64_t step_delta;       // steps to simulate in this launch
+    int32_t* lst_f;           // [G*list_cap] event path, list profile: planned finishes
+    uint32_t* lst_q;          // [G*list_cap]   and prefix sums of s - k
+    int32_t list_cap;         // entries per segment (bound on concurrent requests)
 };
 
 struct FinArgs {
@@ -120,9 +124,12 @@ hipError_t launch_build_rec(const SortArgs& A, int nchunks, hipStream_t s);
 enum { SORT_REC_MAX = 8192 };
 hipError_t prepare_sort_rec(int max_n);
 hipError_t launch_sort_rec(const SortArgs& A, int G, int max_n, hipStream_t s);
-hipError_t prepare_sim(bool d_lds, size_t lds_bytes);
-hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, size_t lds_bytes,
-                      hipStream_t s);
+hipError_t prepare_sim(bool d_lds, size_t lds_ring, bool list, size_t lds_list);
+// list: the event path keeps its profile as the finish-ordered list
+hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool list,
+                      size_t lds_bytes, hipStream_t s);
+// resident waves per compute unit of the event kernel (ring or list profile)
+hipError_t sim_known_occupancy(bool list, bool d_lds, size_t lds_bytes, int* blocks);
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s);
 
 }  // namespace svfk

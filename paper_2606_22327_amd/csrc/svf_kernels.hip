@@ -133,7 +133,7 @@ __global__ void k_init_state(SegState* __restrict__ st, int32_t G) {
     SegState z;
     z.t = 0; z.cursor = 0; z.seq = 0; z.status = STATUS_RUNNING;
     z.nA = 0; z.nfin = 0; z.max_fin = 0; z.head_rank = -1;
-    z.t_f = 0; z.N_O = 0; z.C_O = 0; z.peak = 0; z.req_steps = 0; z.pad = 0;
+    z.t_f = 0; z.N_O = 0; z.C_O = 0; z.peak = 0; z.req_steps = 0; z.ln = 0; z.lq = 0;
     st[g] = z;
 }
 
@@ -776,16 +776,192 @@ __device__ __forceinline__ void fold_range(const Ring<LDS>& R, int lo, int hi, i
 
 // ---- known lengths: event-driven
 
+// The event path keeps the future memory profile of the running requests in
+// one of two forms (chosen per batch by the host, whichever needs less LDS):
+// the ring of G = D + tau values (RingProf) or a list of the running requests
+// ordered by planned finish (ListProf).  Both offer begin (at each visited
+// step, before admissions), fit (the forward-looking check of a candidate
+// started at t, and its admission when it fits; *t_free as in fit_and_admit
+// otherwise) and end (the peak of the steps up to t).
+
 template <bool LDS>
+struct RingProf {
+    const Ring<LDS>& D;
+    int folded;     // slots of steps <= folded are labelled for the current window
+    int peak_lane;  // per-lane largest memory total of the folded steps
+    __device__ __forceinline__ RingProf(const Ring<LDS>& d, int t) : D(d), folded(t), peak_lane(0) {}
+    __device__ __forceinline__ void begin(int) {}
+    __device__ __forceinline__ bool fit(int t, int s_h, int oh, int M, int maxF, int* t_free) {
+        // slots up to t + oh must be labelled for the current window
+        if (t + oh - D.H > folded) {
+            const int to = min(t, t + oh - D.H + 512);
+            fold_range(D, folded, to, peak_lane);
+            folded = to;
+        }
+        return fit_and_admit(D, t, s_h, oh, M, 0, maxF, t_free);
+    }
+    __device__ __forceinline__ int end(int t) {
+        // every past step folded: the ring is canonical again
+        fold_range(D, folded, t, peak_lane);
+        return wmax(peak_lane);
+    }
+};
+
+// The running requests sorted by planned finish F, latest first (entry 0 has
+// the largest F), with Q_j = sum over the entries 0..j of (s - k) in wrapping
+// 32-bit arithmetic (every quantity formed from it fits in int32).  The memory
+// at step tau is D(tau) = sum over running requests with F >= tau of
+// (s - k + tau).  Between two finish steps it grows with tau, so the check of
+// a candidate (size s_h, planned length oh) started at t needs only the steps
+// tau = F_j <= te = t + oh and tau = te:
+//   D(F_j) + F_j = Q_j + F_j (j + 2)      (the entries 0..j have F >= F_j),
+//   D(te) + te   = Q_{c-1} + te (c + 1)   (c entries have F >= te),
+// each at most M - s_h + t (Appendix E.2, eq:c2).  These are the last entries
+// of the list, read from the end in groups of 64 until an entry with F > te
+// shows up; a short candidate touches one group.  Admission inserts the
+// candidate at c: the entries behind it move up by one and gain s_h - t in
+// Q.  Requests finished by t are the last entries and are dropped at each
+// visited step; D at their finish step goes into the peak.  At most cap
+// requests run at once (a bound computed by the host).
+struct ListProf {
+    int32_t* F;     // [cap] planned finish, descending
+    uint32_t* Q;    // [cap] prefix sums of s - k
+    int cap;        // capacity
+    int ln;         // entries
+    uint32_t tot;   // Q of the last entry (0 if none)
+    int peak_lane;
+    __device__ __forceinline__ void begin(int t) {
+        const int lane = lane_id();
+        while (ln > 0) {
+            const int top = ln, base = uni(max(top - 64, 0));
+            const int j = base + lane;
+            const bool valid = j < top;
+            const int f = F[min(j, top - 1)];
+            const uint32_t q = Q[min(j, top - 1)];
+            const bool done = valid && f <= t;
+            const uint64_t dm = ballot(done);
+            if (dm == 0ull) break;
+            // the memory at the finish step of a finished request
+            peak_lane = max(peak_lane, done ? (int)(q + (uint32_t)f * (uint32_t)(j + 1)) : 0);
+            const int nd = __popcll(dm);  // the finished ones end the group
+            ln = uni(top - nd);
+            if (ln > base) {
+                tot = (uint32_t)__builtin_amdgcn_readlane((int)q, ln - 1 - base);
+                break;
+            }
+            if (ln == 0) tot = 0u;
+        }
+    }
+    __device__ __forceinline__ bool fit(int t, int s_h, int oh, int M, int maxF, int* t_free) {
+        (void)maxF;
+        const int lane = lane_id();
+        const int te = t + oh;
+        const int X = M - s_h;
+        const int lim = X + t;
+        // groups of 64 entries from the end, down to the one holding an entry
+        // with F > te (or the first entry)
+        int m = INT32_MIN;
+        int top = ln, base = 0, f = 0, j = 0;
+        uint32_t q = 0u;
+        bool valid = false;
+        int ngroups = 0;
+        for (;;) {
+            base = uni(max(top - 64, 0));
+            j = base + lane;
+            valid = j < top;
+            f = F[min(j, max(top - 1, 0))];
+            q = Q[min(j, max(top - 1, 0))];
+            const bool in = valid && f <= te;
+            m = max(m, in ? (int)(q + (uint32_t)f * (uint32_t)(j + 2)) : INT32_MIN);
+            ++ngroups;
+            if (ballot(valid && f > te) != 0ull || base == 0) break;
+            top = base;
+        }
+        const int c = uni(base + __popcll(ballot(valid && f >= te)));
+        const uint32_t qc1 = c > base ? (uint32_t)__builtin_amdgcn_readlane((int)q, c - 1 - base) : 0u;
+        const int ve = (int)(qc1 + (uint32_t)te * (uint32_t)(c + 1));
+        m = max(m, ve);
+        if (ballot(m > lim) != 0ull) {
+            // the release step: max over the violating steps of min(tau, D + tau - X)
+            int rel = min(te, ve - X);
+            if (ngroups == 1) {
+                const bool in = valid && f <= te;
+                const int v = (int)(q + (uint32_t)f * (uint32_t)(j + 2));
+                rel = max(rel, in ? min(f, v - X) : INT32_MIN);
+            } else {
+                // the same groups again (base: the lowest one scanned)
+                for (int tp = ln;;) {
+                    const int b = uni(max(tp - 64, 0));
+                    const int jj = b + lane;
+                    const bool vv = jj < tp;
+                    const int ff = F[min(jj, tp - 1)];
+                    const uint32_t qq = Q[min(jj, tp - 1)];
+                    const bool in = vv && ff <= te;
+                    const int v = (int)(qq + (uint32_t)ff * (uint32_t)(jj + 2));
+                    rel = max(rel, in ? min(ff, v - X) : INT32_MIN);
+                    if (b <= base) break;
+                    tp = b;
+                }
+            }
+            *t_free = wmax(rel);
+            return false;
+        }
+        // admission: the entries c .. ln-1 (F < te) move up by one.  (The
+        // host's bound keeps ln < cap; were it wrong, the candidate would
+        // stay blocked and the segment end as exhausted.)
+        if (ln >= cap) {
+            *t_free = INT32_MAX;
+            return false;
+        }
+        const uint32_t ch = (uint32_t)(s_h - t);
+        if (ngroups == 1) {
+            if (valid && j >= c) {
+                F[j + 1] = f;
+                Q[j + 1] = q + ch;
+            }
+        } else {
+            // groups from the end, so that no entry is overwritten unread
+            for (int tp = ln;;) {
+                const int b = uni(max(tp - 64, 0));
+                const int jj = b + lane;
+                const bool vv = jj < tp;
+                const int ff = F[min(jj, tp - 1)];
+                const uint32_t qq = Q[min(jj, tp - 1)];
+                if (vv && jj >= c) {
+                    F[jj + 1] = ff;
+                    Q[jj + 1] = qq + ch;
+                }
+                lds_order();
+                if (b <= c) break;
+                tp = b;
+            }
+        }
+        if (lane == 0) {
+            F[c] = te;
+            Q[c] = qc1 + ch;
+        }
+        lds_order();
+        ++ln;
+        tot += ch;
+        return true;
+    }
+    __device__ __forceinline__ int end(int t) {
+        begin(t);
+        // the memory at step t of the requests still running
+        if (ln > 0) peak_lane = max(peak_lane, (int)(tot + (uint32_t)t * (uint32_t)ln));
+        return wmax(peak_lane);
+    }
+};
+
+
+template <class PROF>
 __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
-                          const Ring<LDS>& D, SegState& st, int t_lim) {
+                          PROF& prof, SegState& st, int t_lim) {
     const int lane = lane_id();
     const int M = P.M;
     const int n = sg.n;
     int t = uni(st.t), cursor = uni(st.cursor), seq = uni(st.seq), nadm = uni(st.nfin);
     int max_fin = uni(st.max_fin), head = uni(st.head_rank), t_f = uni(st.t_f);
-    int peak_lane = 0;
-    int folded = t;  // slots of steps <= folded are labelled for the current window
     int status = STATUS_RUNNING;
 
     // Arrival window: lane l holds request wb + l (arrival, rank, record).
@@ -888,15 +1064,10 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
             int4 q = hq;
             if (new_min < old_head) { r = new_min; q = nq; }
             load_word(r >> 6);  // arrivals may have changed any word
+            prof.begin(t);
             for (;;) {
                 int tf = 0;
-                // slots up to t + oh must be labelled for the current window
-                if (t + q.z - D.H > folded) {
-                    const int to = min(t, t + q.z - D.H + 512);
-                    fold_range(D, folded, to, peak_lane);
-                    folded = to;
-                }
-                if (!fit_and_admit(D, t, q.y, q.z, M, 0, max_fin, &tf)) { head = r; hq = q; t_f = tf; break; }
+                if (!prof.fit(t, q.y, q.z, M, max_fin, &tf)) { head = r; hq = q; t_f = tf; break; }
                 if (lane == nstg) {
                     stg_idx = q.x;
                     stg_t = t;
@@ -948,11 +1119,11 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         t = uni(nt);
     }
     flush();
-    // every past step folded: the ring is canonical again and the peak complete
-    fold_range(D, folded, t, peak_lane);
+    // the peak over the steps up to t
+    const int pk = prof.end(t);
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nadm; st.max_fin = max_fin;
     st.head_rank = head; st.t_f = t_f; st.status = status;
-    st.peak = max(st.peak, (int64_t)wmax(peak_lane));
+    st.peak = max(st.peak, (int64_t)pk);
 }
 
 // ---- planned lengths differ from the truth: one step at a time
@@ -1225,8 +1396,10 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
 
 // One wave64 per segment; launched once for segments that plan with the
 // true lengths (event-driven) and once for the others (per step), so each
-// kernel carries only its own path.
-template <bool D_LDS, bool STEPPED>
+// kernel carries only its own path.  LIST: the event path keeps its profile
+// as the finish-ordered list (LDS after the bitmap, kept in global memory
+// between launches) instead of the ring.
+template <bool D_LDS, bool STEPPED, bool LIST>
 __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     extern __shared__ uint64_t smem[];
     const int g = blockIdx.x;
@@ -1261,35 +1434,61 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     uint64_t* S = smem + W0;
     for (int x = lane; x < W0 + W1; x += 64) B[x] = Bg[x];
 
-    const int RS = P.H + 64;  // ring stride: H slots and the spare slot, padded
-    int32_t* Dg = P.ring + (int64_t)g * RS;
-    int32_t* Dl = reinterpret_cast<int32_t*>(smem + P.bw_max);
-    if (D_LDS) {
-        for (int x = lane; x < P.H; x += 64) Dl[x] = Dg[x];
-    }
-    __syncthreads();
-
     // steps t < t_lim are simulated in this launch
     const int64_t want = (int64_t)st.t + P.step_delta;
     const int t_lim = (int)min(want, (int64_t)P.max_steps + 2);
 
-    Ring<D_LDS> D;
-    D.p = D_LDS ? Dl : Dg;
-    D.H = P.H;
-    D.mask = P.H - 1;
-    if (STEPPED) {
-        RunList L;
-        L.q = sg.act;
-        L.kr = sg.actkr;
-        run_stepped(P, sg, B, S, W1, D, L, st, t_lim);
+    if (LIST) {
+        const int cap = P.list_cap;
+        int32_t* Fg = P.lst_f + (int64_t)g * cap;
+        uint32_t* Qg = P.lst_q + (int64_t)g * cap;
+        ListProf L;
+        L.cap = cap;
+        L.F = reinterpret_cast<int32_t*>(smem + P.bw_max);
+        L.Q = reinterpret_cast<uint32_t*>(L.F + cap);
+        L.ln = uni(st.ln);
+        L.tot = (uint32_t)uni((int)st.lq);
+        L.peak_lane = 0;
+        for (int x = lane; x < L.ln; x += 64) {
+            L.F[x] = Fg[x];
+            L.Q[x] = Qg[x];
+        }
+        __syncthreads();
+        run_known(P, sg, B, S, W1, L, st, t_lim);
+        __syncthreads();
+        for (int x = lane; x < L.ln; x += 64) {
+            Fg[x] = L.F[x];
+            Qg[x] = L.Q[x];
+        }
+        st.ln = L.ln;
+        st.lq = L.tot;
     } else {
-        run_known(P, sg, B, S, W1, D, st, t_lim);
+        const int RS = P.H + 64;  // ring stride: H slots and the spare slot, padded
+        int32_t* Dg = P.ring + (int64_t)g * RS;
+        int32_t* Dl = reinterpret_cast<int32_t*>(smem + P.bw_max);
+        if (D_LDS) {
+            for (int x = lane; x < P.H; x += 64) Dl[x] = Dg[x];
+        }
+        __syncthreads();
+        Ring<D_LDS> D;
+        D.p = D_LDS ? Dl : Dg;
+        D.H = P.H;
+        D.mask = P.H - 1;
+        if (STEPPED) {
+            RunList A;
+            A.q = sg.act;
+            A.kr = sg.actkr;
+            run_stepped(P, sg, B, S, W1, D, A, st, t_lim);
+        } else {
+            RingProf<D_LDS> R(D, uni(st.t));
+            run_known(P, sg, B, S, W1, R, st, t_lim);
+        }
+        __syncthreads();
+        if (D_LDS) {
+            for (int x = lane; x < P.H; x += 64) Dg[x] = Dl[x];
+        }
     }
-    __syncthreads();
     for (int x = lane; x < W0 + W1; x += 64) Bg[x] = B[x];
-    if (D_LDS) {
-        for (int x = lane; x < P.H; x += 64) Dg[x] = Dl[x];
-    }
     if (lane == 0) P.st[g] = st;
 }
 
@@ -1437,35 +1636,46 @@ hipError_t launch_sort_rec(const SortArgs& A, int G, int max_n, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, size_t lds_bytes,
-                      hipStream_t s) {
+hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool list,
+                      size_t lds_bytes, hipStream_t s) {
     if (G <= 0) return hipSuccess;
-    if (d_lds) {
-        if (stepped) hipLaunchKernelGGL((k_sim<true, true>), dim3(G), dim3(64), lds_bytes, s, P);
-        else hipLaunchKernelGGL((k_sim<true, false>), dim3(G), dim3(64), lds_bytes, s, P);
+    if (!stepped && list) {
+        hipLaunchKernelGGL((k_sim<false, false, true>), dim3(G), dim3(64), lds_bytes, s, P);
+    } else if (d_lds) {
+        if (stepped) hipLaunchKernelGGL((k_sim<true, true, false>), dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL((k_sim<true, false, false>), dim3(G), dim3(64), lds_bytes, s, P);
     } else {
-        if (stepped) hipLaunchKernelGGL((k_sim<false, true>), dim3(G), dim3(64), lds_bytes, s, P);
-        else hipLaunchKernelGGL((k_sim<false, false>), dim3(G), dim3(64), lds_bytes, s, P);
+        if (stepped) hipLaunchKernelGGL((k_sim<false, true, false>), dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL((k_sim<false, false, false>), dim3(G), dim3(64), lds_bytes, s, P);
     }
     return hipGetLastError();
 }
 
-hipError_t prepare_sim(bool d_lds, size_t lds_bytes) {
+static hipError_t sim_attr(const void* f, size_t lds_bytes) {
     if (lds_bytes <= 65536) return hipSuccess;
-    const void* fns[2];
+    return hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_bytes);
+}
+
+hipError_t prepare_sim(bool d_lds, size_t lds_ring, bool list, size_t lds_list) {
+    hipError_t e;
     if (d_lds) {
-        fns[0] = (const void*)k_sim<true, true>;
-        fns[1] = (const void*)k_sim<true, false>;
+        e = sim_attr((const void*)k_sim<true, true, false>, lds_ring);
+        if (e == hipSuccess) e = sim_attr((const void*)k_sim<true, false, false>, lds_ring);
     } else {
-        fns[0] = (const void*)k_sim<false, true>;
-        fns[1] = (const void*)k_sim<false, false>;
+        e = sim_attr((const void*)k_sim<false, true, false>, lds_ring);
+        if (e == hipSuccess) e = sim_attr((const void*)k_sim<false, false, false>, lds_ring);
     }
-    for (const void* f : fns) {
-        hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)lds_bytes);
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
+    if (e == hipSuccess && list) e = sim_attr((const void*)k_sim<false, false, true>, lds_list);
+    return e;
+}
+
+hipError_t sim_known_occupancy(bool list, bool d_lds, size_t lds_bytes, int* blocks) {
+    const void* f = list ? (const void*)k_sim<false, false, true>
+                         : (d_lds ? (const void*)k_sim<true, false, false>
+                                  : (const void*)k_sim<false, false, false>);
+    hipError_t e = sim_attr(f, lds_bytes);
+    if (e != hipSuccess) return e;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, f, 64, lds_bytes);
 }
 
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s) {

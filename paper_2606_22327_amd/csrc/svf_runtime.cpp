@@ -61,6 +61,10 @@ struct svf_batch {
     std::vector<int64_t> offsets;
     int32_t H = 1, CH = 64, nchunks = 0, bw_max = 0, max_n = 0;
     bool fused_sort = false;  // every instance fits one workgroup of k_sort_rec
+    bool list_known = false;  // event path: profile as the finish-ordered list
+    bool ring_used = true;    // some segment keeps its profile in the ring
+    int32_t list_cap = 0;     // list entries per segment
+    size_t lds_list = 0;      // LDS of the event kernel with the list
     int32_t kbits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t bw_total = 0;
     bool d_lds = true;
@@ -93,6 +97,8 @@ struct svf_batch {
     SegState* d_st = nullptr;
     int32_t* d_fin_out = nullptr;
     StatsOut* d_stats = nullptr;
+    int32_t* d_lst_f = nullptr;
+    uint32_t* d_lst_q = nullptr;
     const uint64_t* sorted_keys = nullptr;  // which key buffer holds the final order
 };
 
@@ -116,7 +122,7 @@ void free_all(svf_batch* h) {
                     h->d_chunk_seg, h->d_chunk_lo, h->d_keys0, h->d_keys1, h->d_rec,
                     h->d_rank, h->d_stepped, h->d_bw_off, h->d_bitmap, h->d_ring,
                     h->d_start, h->d_fin, h->d_pre, h->d_seq, h->d_act, h->d_actkr, h->d_evl,
-                    h->d_st, h->d_fin_out, h->d_stats};
+                    h->d_st, h->d_fin_out, h->d_stats, h->d_lst_f, h->d_lst_q};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     for (auto& t : h->timed) {
@@ -143,6 +149,33 @@ struct HostView {
     const int32_t *a, *s, *o, *plan;
     const int8_t* bit;
 };
+
+// Largest number of requests of one instance that can run at the same time.
+// A running request holds at least s + 1 tokens at the next step, and the
+// planned (and true) total of that step stays <= M once a step's admissions
+// are done, so at most the k smallest values of s + 1 fit.  Values at or
+// above kCap count as kCap (a lower bound on each), which keeps k an upper
+// bound.
+int64_t running_bound(const int32_t* s, const std::vector<int64_t>& off, int64_t M) {
+    const int kCap = 4096;
+    std::vector<int64_t> h(kCap + 1);
+    int64_t best = 0;
+    for (size_t i = 0; i + 1 < off.size(); ++i) {
+        std::fill(h.begin(), h.end(), 0);
+        for (int64_t j = off[i]; j < off[i + 1]; ++j)
+            h[std::min<int64_t>((int64_t)s[j] + 1, kCap)] += 1;
+        int64_t sum = 0, k = 0;
+        for (int v = 1; v <= kCap; ++v) {
+            if (!h[v]) continue;
+            const int64_t take = std::min<int64_t>(h[v], (M - sum) / v);
+            k += take;
+            sum += take * v;
+            if (take < h[v]) break;
+        }
+        best = std::max(best, k);
+    }
+    return best;
+}
 
 // Everything that can be checked without a GPU.
 int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64_t>& off,
@@ -263,7 +296,8 @@ int do_reset(svf_batch* h) {
     record(h, 0, &e0);
     HIPCHK(svfk::launch_init_state(h->d_st, G, h->stream));
     HIPCHK(svfk::launch_fill_u64(h->d_bitmap, (int64_t)h->P * h->bw_total, 0ull, h->stream));
-    HIPCHK(svfk::launch_init_ring(h->d_ring, (int64_t)G * (h->H + 64), h->H, h->stream));
+    if (h->ring_used)
+        HIPCHK(svfk::launch_init_ring(h->d_ring, (int64_t)G * (h->H + 64), h->H, h->stream));
     if (!h->fused_sort) {
         HIPCHK(svfk::launch_fill_i32(h->d_start, PN, -1, h->stream));
         HIPCHK(svfk::launch_fill_i32(h->d_fin, PN, -1, h->stream));
@@ -339,12 +373,16 @@ int do_sim(svf_batch* h, int64_t delta) {
     S.M = h->M;
     S.max_steps = h->max_steps;
     S.step_delta = delta;
+    S.lst_f = h->d_lst_f;
+    S.lst_q = h->d_lst_q;
+    S.list_cap = h->list_cap;
     hipEvent_t e0 = nullptr;
     record(h, 1, &e0);
     if (h->n_known > 0)
-        HIPCHK(svfk::launch_sim(S, G, h->d_lds, false, h->lds_bytes, h->stream));
+        HIPCHK(svfk::launch_sim(S, G, h->d_lds, false, h->list_known,
+                                h->list_known ? h->lds_list : h->lds_bytes, h->stream));
     if (h->n_stepped > 0)
-        HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, h->lds_bytes, h->stream));
+        HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, false, h->lds_bytes, h->stream));
     record_end(h, 1, e0);
     h->sim_launches += 1;
     h->dirty = true;
@@ -475,6 +513,32 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     if (env && !strcmp(env, "global")) h->d_lds = false;
     if (env && !strcmp(env, "lds") && ring_bytes + bm_bytes <= 160 * 1024) h->d_lds = true;
     h->lds_bytes = std::max<size_t>(8, bm_bytes + (h->d_lds ? ring_bytes : 0));
+    // The event path keeps its profile as the finish-ordered list (8 bytes
+    // per possible running request) in LDS when the ring does not fit there,
+    // or when the ring's LDS is what limits the waves resident on a compute
+    // unit and the list lets more of them reside. Where registers bind the
+    // ring kernel, the ring's shorter per-event work wins.
+    if (h->n_known > 0) {
+        const int64_t cap = std::max<int64_t>(1, running_bound(v.s, off, d->M));
+        const size_t with_list = bm_bytes + (size_t)cap * 8;
+        const char* pe = getenv("SVFSIM_PROFILE");
+        bool use = false;
+        if (with_list <= 64 * 1024) {
+            int w_ring = 0, w_regs = 0, w_list = 0;
+            if (svfk::sim_known_occupancy(false, h->d_lds, h->lds_bytes, &w_ring) == hipSuccess &&
+                svfk::sim_known_occupancy(false, h->d_lds, bm_bytes, &w_regs) == hipSuccess &&
+                svfk::sim_known_occupancy(true, false, with_list, &w_list) == hipSuccess)
+                use = !h->d_lds || (w_ring < w_regs && w_list > w_ring);
+        }
+        if (pe && !strcmp(pe, "ring")) use = false;
+        if (pe && !strcmp(pe, "list")) use = with_list <= 160 * 1024;
+        if (use) {
+            h->list_known = true;
+            h->list_cap = (int32_t)cap;
+            h->lds_list = with_list;
+            h->ring_used = h->any_stepped;
+        }
+    }
     if (h->lds_bytes > 160 * 1024) {
         delete h;
         return fail(SVF_EINVAL, "an instance's rank bitmap needs %zu bytes of LDS (> 160 KB)", h->lds_bytes);
@@ -503,7 +567,11 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     ALLOC(d_stepped, G);
     ALLOC(d_bw_off, I + 1);
     ALLOC(d_bitmap, (int64_t)P * h->bw_total);
-    ALLOC(d_ring, G * (h->H + 64));
+    if (h->ring_used) ALLOC(d_ring, G * (h->H + 64));
+    if (h->list_known) {
+        ALLOC(d_lst_f, G * (int64_t)h->list_cap);
+        ALLOC(d_lst_q, G * (int64_t)h->list_cap);
+    }
     ALLOC(d_start, PN);
     ALLOC(d_fin, PN);
     ALLOC(d_pre, PN);
@@ -540,7 +608,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
 #undef CPY
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess) {
-        hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes);
+        hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes, h->list_known, h->lds_list);
         if (a != hipSuccess) e = a;
     }
     if (e == hipSuccess && h->fused_sort) {

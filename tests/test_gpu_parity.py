@@ -287,6 +287,34 @@ def test_stepped_many_concurrent_tiny_prompts():
         compare(b, g[pol], pol, label="tinyprompts")
 
 
+@pytest.mark.parametrize("profile", ["ring", "list"])
+def test_event_path_both_profiles(profile):
+    """The event path keeps the future memory profile either as the ring of
+    G = D + tau or as the finish-ordered list (the host picks the one needing
+    less LDS).  Each forced on the same batches, against the oracle: burst and
+    online instances, ragged sizes, a step-by-step run with partial reads."""
+    os.environ["SVFSIM_PROFILE"] = profile
+    try:
+        b = W.config(2, instances=12, n=400)
+        say(f"profile {profile}: config 2 reduced")
+        g = gpu_run(b)
+        for pol in b.policies:
+            compare(b, g[pol], pol, label=f"{profile}-cfg2")
+        b1 = W.config(1, instances=64)
+        g1 = gpu_run(b1)
+        for pol in b1.policies:
+            compare(b1, g1[pol], pol, label=f"{profile}-cfg1")
+        b4 = W.config(4, instances=6, n=1500)
+        g4 = gpu_run(b4, chunks=[97, 1, 1000, 5, 4000, 1 << 20])
+        compare(b4, g4["svf"], "svf", label=f"{profile}-cfg4-chunked")
+        r = W.random_small(5, instances=40, n_max=120, s_max=30, o_max=90, M=300, gap_mean=0.8)
+        gr = gpu_run(r, ("svf", "sjf", "fcfs"))
+        for pol in ("svf", "sjf", "fcfs"):
+            compare(r, gr[pol], pol, label=f"{profile}-random")
+    finally:
+        del os.environ["SVFSIM_PROFILE"]
+
+
 def test_degenerate_cases():
     say("degenerate cases")
     # all instances empty
