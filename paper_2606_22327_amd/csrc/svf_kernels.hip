@@ -777,7 +777,7 @@ __device__ __forceinline__ void fold_range(const Ring<LDS>& R, int lo, int hi, i
 // ---- known lengths: event-driven
 
 // The event path keeps the future memory profile of the running requests in
-// one of two forms (chosen per batch by the host, whichever needs less LDS):
+// one of two forms (chosen per batch by the host from the LDS each needs):
 // the ring of G = D + tau values (RingProf) or a list of the running requests
 // ordered by planned finish (ListProf).  Both offer begin (at each visited
 // step, before admissions), fit (the forward-looking check of a candidate
@@ -808,10 +808,10 @@ struct RingProf {
 };
 
 // The running requests sorted by planned finish F, latest first (entry 0 has
-// the largest F), with Q_j = sum over the entries 0..j of (s - k) in wrapping
-// 32-bit arithmetic (every quantity formed from it fits in int32).  The memory
-// at step tau is D(tau) = sum over running requests with F >= tau of
-// (s - k + tau).  Between two finish steps it grows with tau, so the check of
+// the largest F), with Q_j = sum over the entries 0..j of (s - k), k the step a
+// request was started at, in wrapping 32-bit arithmetic (every quantity formed
+// from it fits in int32).  The memory at step tau is D(tau) = sum over running
+// requests with F >= tau of (s - k + tau).  Between two finish steps it grows with tau, so the check of
 // a candidate (size s_h, planned length oh) started at t needs only the steps
 // tau = F_j <= te = t + oh and tau = te:
 //   D(F_j) + F_j = Q_j + F_j (j + 2)      (the entries 0..j have F >= F_j),
