@@ -28,6 +28,8 @@ struct SegState {
     int64_t req_steps;  // per-step path: sum over steps of running requests
     int32_t ln;         // event path with the list profile: running requests
     uint32_t lq;        //   and the prefix sum of (s - k) of the last entry
+    int32_t resume_lim; // list full before step resume_lim: continue up to there (0: no)
+    int32_t pad;
 };
 
 // Same layout as svf_instance_stats of the public header.
@@ -92,9 +94,11 @@ struct SimArgs {
     int32_t M;
     int32_t max_steps;
     int64_t step_delta;       // steps to simulate in this launch
-    int32_t* lst_f;           // [G*list_cap] event path, list profile: planned finishes
-    uint32_t* lst_q;          // [G*list_cap]   and prefix sums of s - k
-    int32_t list_cap;         // entries per segment (bound on concurrent requests)
+    int32_t* lst_f;           // [G*list_stride] event path, list profile: planned finishes
+    uint32_t* lst_q;          // [G*list_stride]   and prefix sums of s - k
+    int32_t list_stride;      // entries per segment in HBM (bound on concurrent requests)
+    int32_t list_cap;         // entries per segment in LDS in this launch (<= list_stride)
+    int32_t list_resume;      // 1: only continue the segments that stopped with a full list
 };
 
 struct FinArgs {

@@ -134,6 +134,7 @@ __global__ void k_init_state(SegState* __restrict__ st, int32_t G) {
     z.t = 0; z.cursor = 0; z.seq = 0; z.status = STATUS_RUNNING;
     z.nA = 0; z.nfin = 0; z.max_fin = 0; z.head_rank = -1;
     z.t_f = 0; z.N_O = 0; z.C_O = 0; z.peak = 0; z.req_steps = 0; z.ln = 0; z.lq = 0;
+    z.resume_lim = 0; z.pad = 0;
     st[g] = z;
 }
 
@@ -782,7 +783,8 @@ __device__ __forceinline__ void fold_range(const Ring<LDS>& R, int lo, int hi, i
 // ordered by planned finish (ListProf).  Both offer begin (at each visited
 // step, before admissions), fit (the forward-looking check of a candidate
 // started at t, and its admission when it fits; *t_free as in fit_and_admit
-// otherwise) and end (the peak of the steps up to t).
+// otherwise), stopped (the segment has to leave the launch at the current
+// step) and end (the peak of the steps up to t).
 
 template <bool LDS>
 struct RingProf {
@@ -791,6 +793,7 @@ struct RingProf {
     int peak_lane;  // per-lane largest memory total of the folded steps
     __device__ __forceinline__ RingProf(const Ring<LDS>& d, int t) : D(d), folded(t), peak_lane(0) {}
     __device__ __forceinline__ void begin(int) {}
+    __device__ __forceinline__ bool stopped() const { return false; }
     __device__ __forceinline__ bool fit(int t, int s_h, int oh, int M, int maxF, int* t_free) {
         // slots up to t + oh must be labelled for the current window
         if (t + oh - D.H > folded) {
@@ -821,8 +824,11 @@ struct RingProf {
 // shows up; a short candidate touches one group.  Admission inserts the
 // candidate at c: the entries behind it move up by one and gain s_h - t in
 // Q.  Requests finished by t are the last entries and are dropped at each
-// visited step; D at their finish step goes into the peak.  At most cap
-// requests run at once (a bound computed by the host).
+// visited step; D at their finish step goes into the peak.  The host bounds
+// the requests that can run at once; the list in LDS may hold fewer (more
+// waves then fit on a compute unit).  A candidate that fits into a full list
+// stops the segment at that step (stopped(), with the candidate as the head
+// and t_f = t); a later launch with room for the bound continues it.
 struct ListProf {
     int32_t* F;     // [cap] planned finish, descending
     uint32_t* Q;    // [cap] prefix sums of s - k
@@ -830,6 +836,9 @@ struct ListProf {
     int ln;         // entries
     uint32_t tot;   // Q of the last entry (0 if none)
     int peak_lane;
+    bool may_stop;  // a full list stops the segment (else: the bound was wrong)
+    bool full;      // stopped on a full list
+    __device__ __forceinline__ bool stopped() const { return full; }
     __device__ __forceinline__ void begin(int t) {
         const int lane = lane_id();
         while (ln > 0) {
@@ -906,11 +915,13 @@ struct ListProf {
             *t_free = wmax(rel);
             return false;
         }
-        // admission: the entries c .. ln-1 (F < te) move up by one.  (The
-        // host's bound keeps ln < cap; were it wrong, the candidate would
-        // stay blocked and the segment end as exhausted.)
+        // admission: the entries c .. ln-1 (F < te) move up by one.  With
+        // room for the host's bound the list is never full here; were the
+        // bound wrong, the candidate would stay blocked and the segment end
+        // as exhausted.
         if (ln >= cap) {
-            *t_free = INT32_MAX;
+            full = may_stop;
+            *t_free = may_stop ? t : INT32_MAX;
             return false;
         }
         const uint32_t ch = (uint32_t)(s_h - t);
@@ -1104,6 +1115,9 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                 q = rec_of(r);
             }
         }
+
+        // the candidate is the head, checked again at t when the segment resumes
+        if (prof.stopped()) break;
 
         // 5. advance to the next step where anything can happen
         const int next_arr = cursor < wb + 64 ? __builtin_amdgcn_readlane(a_reg, cursor - wb)
@@ -1410,6 +1424,7 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     const int n = (int)(P.offsets[inst + 1] - off);
     SegState st = P.st[g];
     if (st.status != STATUS_RUNNING) return;
+    if (LIST && P.list_resume && st.resume_lim == 0) return;
 
     Seg sg;
     sg.n = n;
@@ -1436,12 +1451,12 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
 
     // steps t < t_lim are simulated in this launch
     const int64_t want = (int64_t)st.t + P.step_delta;
-    const int t_lim = (int)min(want, (int64_t)P.max_steps + 2);
+    int t_lim = (int)min(want, (int64_t)P.max_steps + 2);
 
     if (LIST) {
         const int cap = P.list_cap;
-        int32_t* Fg = P.lst_f + (int64_t)g * cap;
-        uint32_t* Qg = P.lst_q + (int64_t)g * cap;
+        int32_t* Fg = P.lst_f + (int64_t)g * P.list_stride;
+        uint32_t* Qg = P.lst_q + (int64_t)g * P.list_stride;
         ListProf L;
         L.cap = cap;
         L.F = reinterpret_cast<int32_t*>(smem + P.bw_max);
@@ -1449,19 +1464,29 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
         L.ln = uni(st.ln);
         L.tot = (uint32_t)uni((int)st.lq);
         L.peak_lane = 0;
-        for (int x = lane; x < L.ln; x += 64) {
-            L.F[x] = Fg[x];
-            L.Q[x] = Qg[x];
+        L.may_stop = cap < P.list_stride;
+        L.full = false;
+        if (P.list_resume) t_lim = st.resume_lim;
+        st.resume_lim = 0;
+        if (L.ln > cap) {
+            // more running than this launch has room for: left to the continuation
+            st.resume_lim = t_lim;
+        } else {
+            for (int x = lane; x < L.ln; x += 64) {
+                L.F[x] = Fg[x];
+                L.Q[x] = Qg[x];
+            }
+            __syncthreads();
+            run_known(P, sg, B, S, W1, L, st, t_lim);
+            __syncthreads();
+            for (int x = lane; x < L.ln; x += 64) {
+                Fg[x] = L.F[x];
+                Qg[x] = L.Q[x];
+            }
+            st.ln = L.ln;
+            st.lq = L.tot;
+            if (L.full) st.resume_lim = t_lim;
         }
-        __syncthreads();
-        run_known(P, sg, B, S, W1, L, st, t_lim);
-        __syncthreads();
-        for (int x = lane; x < L.ln; x += 64) {
-            Fg[x] = L.F[x];
-            Qg[x] = L.Q[x];
-        }
-        st.ln = L.ln;
-        st.lq = L.tot;
     } else {
         const int RS = P.H + 64;  // ring stride: H slots and the spare slot, padded
         int32_t* Dg = P.ring + (int64_t)g * RS;

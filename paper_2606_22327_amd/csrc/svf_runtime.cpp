@@ -17,7 +17,7 @@ using svfk::SegState;
 using svfk::StatsOut;
 
 static_assert(sizeof(StatsOut) == sizeof(svf_instance_stats), "stats layout");
-static_assert(sizeof(SegState) == 72, "state layout");
+static_assert(sizeof(SegState) == 80, "state layout");
 
 namespace {
 
@@ -63,8 +63,10 @@ struct svf_batch {
     bool fused_sort = false;  // every instance fits one workgroup of k_sort_rec
     bool list_known = false;  // event path: profile as the finish-ordered list
     bool ring_used = true;    // some segment keeps its profile in the ring
-    int32_t list_cap = 0;     // list entries per segment
+    int32_t list_stride = 0;  // list entries per segment in HBM (the bound)
+    int32_t list_cap = 0;     // list entries per segment in LDS (first launch)
     size_t lds_list = 0;      // LDS of the event kernel with the list
+    size_t lds_list_full = 0; //   and with room for the bound (continuation)
     int32_t kbits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t bw_total = 0;
     bool d_lds = true;
@@ -375,12 +377,21 @@ int do_sim(svf_batch* h, int64_t delta) {
     S.step_delta = delta;
     S.lst_f = h->d_lst_f;
     S.lst_q = h->d_lst_q;
+    S.list_stride = h->list_stride;
     S.list_cap = h->list_cap;
+    S.list_resume = 0;
     hipEvent_t e0 = nullptr;
     record(h, 1, &e0);
-    if (h->n_known > 0)
+    if (h->n_known > 0) {
         HIPCHK(svfk::launch_sim(S, G, h->d_lds, false, h->list_known,
                                 h->list_known ? h->lds_list : h->lds_bytes, h->stream));
+        if (h->list_known && h->list_cap < h->list_stride) {
+            // segments whose list outgrew the LDS capacity, up to the same step
+            S.list_cap = h->list_stride;
+            S.list_resume = 1;
+            HIPCHK(svfk::launch_sim(S, G, false, false, true, h->lds_list_full, h->stream));
+        }
+    }
     if (h->n_stepped > 0)
         HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, false, h->lds_bytes, h->stream));
     record_end(h, 1, e0);
@@ -514,28 +525,54 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     if (env && !strcmp(env, "lds") && ring_bytes + bm_bytes <= 160 * 1024) h->d_lds = true;
     h->lds_bytes = std::max<size_t>(8, bm_bytes + (h->d_lds ? ring_bytes : 0));
     // The event path keeps its profile as the finish-ordered list (8 bytes
-    // per possible running request) in LDS when the ring does not fit there,
-    // or when the ring's LDS is what limits the waves resident on a compute
-    // unit and the list lets more of them reside. Where registers bind the
-    // ring kernel, the ring's shorter per-event work wins.
+    // per running request) in LDS when the ring does not fit there, or when
+    // the ring's LDS is what limits the waves resident on a compute unit, the
+    // list lets more of them reside and there are more segments than the
+    // ring lets reside at once.  Elsewhere the ring's shorter per-event work
+    // wins.  The list in LDS gets
+    // the largest capacity that still lets as many waves reside as the list
+    // kernel's registers allow; segments that outgrow it stop, and a second
+    // launch with room for the bound on concurrent requests continues them.
     if (h->n_known > 0) {
-        const int64_t cap = std::max<int64_t>(1, running_bound(v.s, off, d->M));
-        const size_t with_list = bm_bytes + (size_t)cap * 8;
+        const int64_t bound = std::max<int64_t>(1, running_bound(v.s, off, d->M));
+        const size_t full_bytes = bm_bytes + (size_t)bound * 8;
         const char* pe = getenv("SVFSIM_PROFILE");
         bool use = false;
-        if (with_list <= 64 * 1024) {
-            int w_ring = 0, w_regs = 0, w_list = 0;
-            if (svfk::sim_known_occupancy(false, h->d_lds, h->lds_bytes, &w_ring) == hipSuccess &&
-                svfk::sim_known_occupancy(false, h->d_lds, bm_bytes, &w_regs) == hipSuccess &&
-                svfk::sim_known_occupancy(true, false, with_list, &w_list) == hipSuccess)
-                use = !h->d_lds || (w_ring < w_regs && w_list > w_ring);
+        int64_t cap = bound;
+        if (full_bytes <= 160 * 1024) {
+            auto occ = [&](bool list, bool dl, size_t bytes) {
+                int w = 0;
+                return svfk::sim_known_occupancy(list, dl, bytes, &w) == hipSuccess ? w : -1;
+            };
+            const int w_top = occ(true, false, bm_bytes + 64 * 8);
+            int64_t lo = std::min<int64_t>(bound, 64), hi = bound;  // occ(lo) >= w_top
+            while (lo < hi) {
+                const int64_t mid = lo + (hi - lo + 1) / 2;
+                if (occ(true, false, bm_bytes + (size_t)mid * 8) >= w_top) lo = mid;
+                else hi = mid - 1;
+            }
+            cap = lo;
+            const char* pc = getenv("SVFSIM_LIST_LDS_CAP");  // testing: a smaller LDS list
+            if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
+            const int w_ring = occ(false, h->d_lds, h->lds_bytes);
+            const int w_regs = occ(false, h->d_lds, bm_bytes);
+            const int w_list = occ(true, false, bm_bytes + (size_t)cap * 8);
+            int cus = 0;
+            if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess)
+                cus = 0;
+            const int64_t segs = (int64_t)h->n_known;
+            if (w_top > 0 && w_ring >= 0 && w_regs >= 0 && w_list > 0)
+                use = !h->d_lds ||
+                      (w_ring < w_regs && w_list > w_ring && segs > (int64_t)w_ring * cus);
         }
         if (pe && !strcmp(pe, "ring")) use = false;
-        if (pe && !strcmp(pe, "list")) use = with_list <= 160 * 1024;
+        if (pe && !strcmp(pe, "list")) use = full_bytes <= 160 * 1024;
         if (use) {
             h->list_known = true;
+            h->list_stride = (int32_t)bound;
             h->list_cap = (int32_t)cap;
-            h->lds_list = with_list;
+            h->lds_list = bm_bytes + (size_t)cap * 8;
+            h->lds_list_full = full_bytes;
             h->ring_used = h->any_stepped;
         }
     }
@@ -569,8 +606,8 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     ALLOC(d_bitmap, (int64_t)P * h->bw_total);
     if (h->ring_used) ALLOC(d_ring, G * (h->H + 64));
     if (h->list_known) {
-        ALLOC(d_lst_f, G * (int64_t)h->list_cap);
-        ALLOC(d_lst_q, G * (int64_t)h->list_cap);
+        ALLOC(d_lst_f, G * (int64_t)h->list_stride);
+        ALLOC(d_lst_q, G * (int64_t)h->list_stride);
     }
     ALLOC(d_start, PN);
     ALLOC(d_fin, PN);
@@ -608,7 +645,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
 #undef CPY
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess) {
-        hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes, h->list_known, h->lds_list);
+        hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes, h->list_known, h->lds_list_full);
         if (a != hipSuccess) e = a;
     }
     if (e == hipSuccess && h->fused_sort) {

@@ -287,19 +287,45 @@ def test_stepped_many_concurrent_tiny_prompts():
         compare(b, g[pol], pol, label="tinyprompts")
 
 
-@pytest.mark.parametrize("profile", ["ring", "list"])
+def max_concurrent(b, res):
+    """Largest number of requests of one instance running at the same step
+    (started at k, running at the steps k+1 .. finish)."""
+    best = 0
+    for i in range(b.num_instances):
+        lo, hi = b.offsets[i], b.offsets[i + 1]
+        st = res["start"][lo:hi].astype(np.int64)
+        fi = res["finish"][lo:hi].astype(np.int64)
+        ok = st >= 0
+        if not ok.any():
+            continue
+        ev = np.concatenate([st[ok] + 1, fi[ok] + 1])
+        dv = np.concatenate([np.ones(ok.sum(), np.int64), -np.ones(ok.sum(), np.int64)])
+        order = np.lexsort((dv, ev))  # at equal steps the ends (-1) go first
+        best = max(best, int(np.cumsum(dv[order]).max()))
+    return best
+
+
+@pytest.mark.parametrize("profile", ["ring", "list", "list-lds7", "list-lds64"])
 def test_event_path_both_profiles(profile):
     """The event path keeps the future memory profile either as the ring of
-    G = D + tau or as the finish-ordered list (the host picks the one needing
-    less LDS).  Each forced on the same batches, against the oracle: burst and
-    online instances, ragged sizes, a step-by-step run with partial reads."""
-    os.environ["SVFSIM_PROFILE"] = profile
+    G = D + tau or as the finish-ordered list (the host picks by LDS and
+    occupancy).  Each forced on the same batches, against the oracle: burst
+    and online instances, ragged sizes, a step-by-step run with partial reads.
+    The list-ldsN cases give the list in LDS room for only N entries, so
+    segments stop when it is full and the continuation launch (room for the
+    host's bound) finishes them, also inside step-by-step runs."""
+    os.environ["SVFSIM_PROFILE"] = profile.split("-")[0]
+    cap = int(profile.split("lds")[1]) if "lds" in profile else None
+    if cap:
+        os.environ["SVFSIM_LIST_LDS_CAP"] = str(cap)
     try:
+        most = 0
         b = W.config(2, instances=12, n=400)
         say(f"profile {profile}: config 2 reduced")
         g = gpu_run(b)
         for pol in b.policies:
             compare(b, g[pol], pol, label=f"{profile}-cfg2")
+            most = max(most, max_concurrent(b, g[pol]))
         b1 = W.config(1, instances=64)
         g1 = gpu_run(b1)
         for pol in b1.policies:
@@ -307,12 +333,16 @@ def test_event_path_both_profiles(profile):
         b4 = W.config(4, instances=6, n=1500)
         g4 = gpu_run(b4, chunks=[97, 1, 1000, 5, 4000, 1 << 20])
         compare(b4, g4["svf"], "svf", label=f"{profile}-cfg4-chunked")
+        most = max(most, max_concurrent(b4, g4["svf"]))
         r = W.random_small(5, instances=40, n_max=120, s_max=30, o_max=90, M=300, gap_mean=0.8)
         gr = gpu_run(r, ("svf", "sjf", "fcfs"))
         for pol in ("svf", "sjf", "fcfs"):
             compare(r, gr[pol], pol, label=f"{profile}-random")
+        if cap:
+            assert most > cap, "no segment outgrew the LDS list: the continuation went untested"
     finally:
         del os.environ["SVFSIM_PROFILE"]
+        os.environ.pop("SVFSIM_LIST_LDS_CAP", None)
 
 
 def test_degenerate_cases():
