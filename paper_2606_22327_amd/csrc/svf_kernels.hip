@@ -3,13 +3,19 @@
 // One "segment" is one instance under one policy; segments are independent.
 // Kernels, in launch order:
 //   k_fill_*          clear state, bitmaps, rings and outputs (no memset nodes)
-//   k_chunk_sort<CH>  priority keys (Eq. 1 / Eq. 2) packed as key<<32|index and
-//                     bitonic-sorted in LDS, one workgroup per chunk of CH
+//   k_sort_rec<NT,E>  instances of at most 8192 requests: priority keys (Eq. 1 /
+//                     Eq. 2), stable radix sort in LDS, rank-ordered records,
+//                     index->rank map and cleared outputs, one workgroup per
+//                     segment; larger instances take the next three kernels
+//   k_chunk_sort<CH>  priority keys packed as key<<32|index and bitonic-sorted
+//                     in LDS, one workgroup per chunk of CH
 //   k_merge_pass      doubles the sorted run length of segments longer than CH
 //                     (each element finds its output slot by binary search in
 //                     the partner run)
 //   k_build_rec       rank-ordered request records and the index->rank map
-//   k_sim<D_LDS>      the simulation: one wave64 per segment
+//   k_sim<D_LDS, STEPPED>, k_sim_list
+//                     the simulation: one wave64 per segment (profile as a ring,
+//                     per-step or event-driven; or as a finish-ordered list)
 //   k_finalize        per-request outputs as of the reached step (finish derived
 //                     as start + o where lengths are known) + per-segment
 //                     statistics
@@ -1414,7 +1420,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
 // as the finish-ordered list (LDS after the bitmap, kept in global memory
 // between launches) instead of the ring.
 template <bool D_LDS, bool STEPPED, bool LIST>
-__global__ __launch_bounds__(64) void k_sim(SimArgs P) {
+__device__ __forceinline__ void sim_segment(const SimArgs& P) {
     extern __shared__ uint64_t smem[];
     const int g = blockIdx.x;
     if ((P.stepped[g] != 0) != STEPPED) return;
@@ -1515,6 +1521,19 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
     }
     for (int x = lane; x < W0 + W1; x += 64) Bg[x] = B[x];
     if (lane == 0) P.st[g] = st;
+}
+
+template <bool D_LDS, bool STEPPED>
+__global__ __launch_bounds__(64) void k_sim(SimArgs P) {
+    sim_segment<D_LDS, STEPPED, false>(P);
+}
+
+// The list kernel needs few vector registers; its scalar state is squeezed
+// (spilled to vector lanes) so that eight waves fit on each SIMD, which the
+// short LDS footprint of the list allows.
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void k_sim_list(SimArgs P) {
+    sim_segment<false, false, true>(P);
 }
 
 // ------------------------------------------------------------ finalize
@@ -1665,13 +1684,13 @@ hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool li
                       size_t lds_bytes, hipStream_t s) {
     if (G <= 0) return hipSuccess;
     if (!stepped && list) {
-        hipLaunchKernelGGL((k_sim<false, false, true>), dim3(G), dim3(64), lds_bytes, s, P);
+        hipLaunchKernelGGL(k_sim_list, dim3(G), dim3(64), lds_bytes, s, P);
     } else if (d_lds) {
-        if (stepped) hipLaunchKernelGGL((k_sim<true, true, false>), dim3(G), dim3(64), lds_bytes, s, P);
-        else hipLaunchKernelGGL((k_sim<true, false, false>), dim3(G), dim3(64), lds_bytes, s, P);
+        if (stepped) hipLaunchKernelGGL((k_sim<true, true>), dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL((k_sim<true, false>), dim3(G), dim3(64), lds_bytes, s, P);
     } else {
-        if (stepped) hipLaunchKernelGGL((k_sim<false, true, false>), dim3(G), dim3(64), lds_bytes, s, P);
-        else hipLaunchKernelGGL((k_sim<false, false, false>), dim3(G), dim3(64), lds_bytes, s, P);
+        if (stepped) hipLaunchKernelGGL((k_sim<false, true>), dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL((k_sim<false, false>), dim3(G), dim3(64), lds_bytes, s, P);
     }
     return hipGetLastError();
 }
@@ -1684,20 +1703,20 @@ static hipError_t sim_attr(const void* f, size_t lds_bytes) {
 hipError_t prepare_sim(bool d_lds, size_t lds_ring, bool list, size_t lds_list) {
     hipError_t e;
     if (d_lds) {
-        e = sim_attr((const void*)k_sim<true, true, false>, lds_ring);
-        if (e == hipSuccess) e = sim_attr((const void*)k_sim<true, false, false>, lds_ring);
+        e = sim_attr((const void*)k_sim<true, true>, lds_ring);
+        if (e == hipSuccess) e = sim_attr((const void*)k_sim<true, false>, lds_ring);
     } else {
-        e = sim_attr((const void*)k_sim<false, true, false>, lds_ring);
-        if (e == hipSuccess) e = sim_attr((const void*)k_sim<false, false, false>, lds_ring);
+        e = sim_attr((const void*)k_sim<false, true>, lds_ring);
+        if (e == hipSuccess) e = sim_attr((const void*)k_sim<false, false>, lds_ring);
     }
-    if (e == hipSuccess && list) e = sim_attr((const void*)k_sim<false, false, true>, lds_list);
+    if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_list, lds_list);
     return e;
 }
 
 hipError_t sim_known_occupancy(bool list, bool d_lds, size_t lds_bytes, int* blocks) {
-    const void* f = list ? (const void*)k_sim<false, false, true>
-                         : (d_lds ? (const void*)k_sim<true, false, false>
-                                  : (const void*)k_sim<false, false, false>);
+    const void* f = list ? (const void*)k_sim_list
+                         : (d_lds ? (const void*)k_sim<true, false>
+                                  : (const void*)k_sim<false, false>);
     hipError_t e = sim_attr(f, lds_bytes);
     if (e != hipSuccess) return e;
     return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, f, 64, lds_bytes);
