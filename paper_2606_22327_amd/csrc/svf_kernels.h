@@ -129,6 +129,8 @@ enum { SORT_REC_MAX = 8192 };
 hipError_t prepare_sort_rec(int max_n);
 hipError_t launch_sort_rec(const SortArgs& A, int G, int max_n, hipStream_t s);
 hipError_t prepare_sim(bool d_lds, size_t lds_ring, bool list, size_t lds_list);
+// entries of LDS the finish-ordered list of capacity cap takes (F and Q each)
+__host__ __device__ inline int list_slots(int cap) { return cap + 65; }
 // list: the event path keeps its profile as the finish-ordered list
 hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool list,
                       size_t lds_bytes, hipStream_t s);

@@ -835,9 +835,19 @@ struct RingProf {
 // waves then fit on a compute unit).  A candidate that fits into a full list
 // stops the segment at that step (stopped(), with the candidate as the head
 // and t_f = t); a later launch with room for the bound continues it.
+//
+// Every lane of a group takes part in every step, so that no lane is masked
+// off (the scalar unit, which would juggle the masks, is the busiest unit of
+// this kernel): lanes past the last entry of a group read a copy of that
+// entry, which leaves maxima unchanged and is taken out of counts, and the
+// shift of an insertion writes each lane's entry to a position of its own (a
+// lane whose entry stays rewrites it in place; the lane of entry c-1 writes
+// the candidate; lanes past the group's end write to a slot of their own
+// behind the capacity, so the arrays have 65 slots more than the list may
+// hold).
 struct ListProf {
-    int32_t* F;     // [cap] planned finish, descending
-    uint32_t* Q;    // [cap] prefix sums of s - k
+    int32_t* F;     // [list_slots(cap)] planned finish, descending
+    uint32_t* Q;    // [list_slots(cap)] prefix sums of s - k
     int cap;        // capacity
     int ln;         // entries
     uint32_t tot;   // Q of the last entry (0 if none)
@@ -848,23 +858,27 @@ struct ListProf {
     __device__ __forceinline__ void begin(int t) {
         const int lane = lane_id();
         while (ln > 0) {
-            const int top = ln, base = uni(max(top - 64, 0));
-            const int j = base + lane;
-            const bool valid = j < top;
-            const int f = F[min(j, top - 1)];
-            const uint32_t q = Q[min(j, top - 1)];
-            const bool done = valid && f <= t;
+            const int top = ln, base = max(top - 64, 0);
+            const int jr = min(base + lane, top - 1);
+            const int f = F[jr];
+            const uint32_t q = Q[jr];
+            const bool done = f <= t;
             const uint64_t dm = ballot(done);
             if (dm == 0ull) break;
             // the memory at the finish step of a finished request
-            peak_lane = max(peak_lane, done ? (int)(q + (uint32_t)f * (uint32_t)(j + 1)) : 0);
-            const int nd = __popcll(dm);  // the finished ones end the group
-            ln = uni(top - nd);
+            peak_lane = max(peak_lane, done ? (int)(q + (uint32_t)f * (uint32_t)(jr + 1)) : 0);
+            // the finished ones end the group; copies of the last entry are
+            // among them
+            ln = top - ((int)__popcll(dm) - (64 - (top - base)));
             if (ln > base) {
                 tot = (uint32_t)__builtin_amdgcn_readlane((int)q, ln - 1 - base);
                 break;
             }
-            if (ln == 0) tot = 0u;
+            if (ln == 0) {
+                tot = 0u;
+                if (lane == 0) F[0] = INT32_MAX;  // an empty list reads as "finishes last"
+                lds_order();
+            }
         }
     }
     __device__ __forceinline__ bool fit(int t, int s_h, int oh, int M, int maxF, int* t_free) {
@@ -874,88 +888,71 @@ struct ListProf {
         const int X = M - s_h;
         const int lim = X + t;
         // groups of 64 entries from the end, down to the one holding an entry
-        // with F > te (or the first entry)
+        // with F > te (its first entry has the largest F) or the first entry
         int m = INT32_MIN;
-        int top = ln, base = 0, f = 0, j = 0;
-        uint32_t q = 0u;
-        bool valid = false;
-        int ngroups = 0;
+        int top = ln, base, f, jr;
+        uint32_t q;
         for (;;) {
-            base = uni(max(top - 64, 0));
-            j = base + lane;
-            valid = j < top;
-            f = F[min(j, max(top - 1, 0))];
-            q = Q[min(j, max(top - 1, 0))];
-            const bool in = valid && f <= te;
-            m = max(m, in ? (int)(q + (uint32_t)f * (uint32_t)(j + 2)) : INT32_MIN);
-            ++ngroups;
-            if (ballot(valid && f > te) != 0ull || base == 0) break;
+            base = max(top - 64, 0);
+            jr = min(base + lane, max(top - 1, 0));
+            f = F[jr];
+            q = Q[jr];
+            m = max(m, f <= te ? (int)(q + (uint32_t)f * (uint32_t)(jr + 2)) : INT32_MIN);
+            if (base == 0) break;
+            if (__builtin_amdgcn_readfirstlane(f) > te) break;
             top = base;
         }
-        const int c = uni(base + __popcll(ballot(valid && f >= te)));
-        const uint32_t qc1 = c > base ? (uint32_t)__builtin_amdgcn_readlane((int)q, c - 1 - base) : 0u;
+        // c = entries with F >= te (a prefix of the group, copies excluded)
+        const int ge = min((int)__popcll(ballot(f >= te)), top - base);
+        const int c = base + ge;
+        const uint32_t qc1 = ge > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)q, ge - 1) : 0u;
         const int ve = (int)(qc1 + (uint32_t)te * (uint32_t)(c + 1));
-        m = max(m, ve);
-        if (ballot(m > lim) != 0ull) {
-            // the release step: max over the violating steps of min(tau, D + tau - X)
+        if (ballot(max(m, ve) > lim) != 0ull) {
+            // the release step: max over the violating steps of min(tau, D + tau - X),
+            // over the same groups again (base: the lowest one scanned)
             int rel = min(te, ve - X);
-            if (ngroups == 1) {
-                const bool in = valid && f <= te;
-                const int v = (int)(q + (uint32_t)f * (uint32_t)(j + 2));
-                rel = max(rel, in ? min(f, v - X) : INT32_MIN);
-            } else {
-                // the same groups again (base: the lowest one scanned)
-                for (int tp = ln;;) {
-                    const int b = uni(max(tp - 64, 0));
-                    const int jj = b + lane;
-                    const bool vv = jj < tp;
-                    const int ff = F[min(jj, tp - 1)];
-                    const uint32_t qq = Q[min(jj, tp - 1)];
-                    const bool in = vv && ff <= te;
-                    const int v = (int)(qq + (uint32_t)ff * (uint32_t)(jj + 2));
-                    rel = max(rel, in ? min(ff, v - X) : INT32_MIN);
-                    if (b <= base) break;
-                    tp = b;
-                }
+            for (int tp = ln;;) {
+                const int b = max(tp - 64, 0);
+                const int jj = min(b + lane, tp - 1);
+                const int ff = F[jj];
+                const int v = (int)(Q[jj] + (uint32_t)ff * (uint32_t)(jj + 2));
+                rel = max(rel, ff <= te ? min(ff, v - X) : INT32_MIN);
+                if (b <= base) break;
+                tp = b;
             }
             *t_free = wmax(rel);
             return false;
         }
-        // admission: the entries c .. ln-1 (F < te) move up by one.  With
-        // room for the host's bound the list is never full here; were the
-        // bound wrong, the candidate would stay blocked and the segment end
-        // as exhausted.
         if (ln >= cap) {
             full = may_stop;
             *t_free = may_stop ? t : INT32_MAX;
             return false;
         }
+        // the entries c .. ln-1 move up by one and gain s_h - t, group by
+        // group from the end (no entry is overwritten unread); entry c-1
+        // writes the candidate behind itself
         const uint32_t ch = (uint32_t)(s_h - t);
-        if (ngroups == 1) {
-            if (valid && j >= c) {
-                F[j + 1] = f;
-                Q[j + 1] = q + ch;
-            }
-        } else {
-            // groups from the end, so that no entry is overwritten unread
-            for (int tp = ln;;) {
-                const int b = uni(max(tp - 64, 0));
-                const int jj = b + lane;
-                const bool vv = jj < tp;
-                const int ff = F[min(jj, tp - 1)];
-                const uint32_t qq = Q[min(jj, tp - 1)];
-                if (vv && jj >= c) {
-                    F[jj + 1] = ff;
-                    Q[jj + 1] = qq + ch;
-                }
-                lds_order();
-                if (b <= c) break;
-                tp = b;
-            }
+        const uint32_t qn = qc1 + ch;
+        for (int tp = ln;;) {
+            const int b = max(tp - 64, 0);
+            const int j = b + lane;
+            const int jj = min(j, max(tp - 1, 0));
+            const int ff = F[jj];
+            const uint32_t qq = Q[jj];
+            const bool mv = j >= c - 1;
+            const bool nw = j == c - 1;
+            // lanes past the group's end: a slot of their own behind the capacity
+            const int pos = j < tp ? (mv ? j + 1 : j) : cap + 1 + lane;
+            F[pos] = nw ? te : ff;
+            Q[pos] = nw ? qn : (mv ? qq + ch : qq);
+            if (b <= c - 1 || b == 0) break;
+            tp = b;
         }
-        if (lane == 0) {
-            F[c] = te;
-            Q[c] = qc1 + ch;
+        if (c == 0) {  // no entry before the candidate
+            if (lane == 0) {
+                F[0] = te;
+                Q[0] = qn;
+            }
         }
         lds_order();
         ++ln;
@@ -1466,7 +1463,7 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
         ListProf L;
         L.cap = cap;
         L.F = reinterpret_cast<int32_t*>(smem + P.bw_max);
-        L.Q = reinterpret_cast<uint32_t*>(L.F + cap);
+        L.Q = reinterpret_cast<uint32_t*>(L.F + list_slots(cap));
         L.ln = uni(st.ln);
         L.tot = (uint32_t)uni((int)st.lq);
         L.peak_lane = 0;
@@ -1482,6 +1479,7 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
                 L.F[x] = Fg[x];
                 L.Q[x] = Qg[x];
             }
+            if (L.ln == 0 && lane == 0) L.F[0] = INT32_MAX;  // the empty list's sentinel
             __syncthreads();
             run_known(P, sg, B, S, W1, L, st, t_lim);
             __syncthreads();

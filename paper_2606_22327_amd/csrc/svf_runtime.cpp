@@ -535,7 +535,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     // launch with room for the bound on concurrent requests continues them.
     if (h->n_known > 0) {
         const int64_t bound = std::max<int64_t>(1, running_bound(v.s, off, d->M));
-        const size_t full_bytes = bm_bytes + (size_t)bound * 8;
+        const size_t full_bytes = bm_bytes + (size_t)svfk::list_slots((int)bound) * 8;
         const char* pe = getenv("SVFSIM_PROFILE");
         bool use = false;
         int64_t cap = bound;
@@ -544,11 +544,11 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
                 int w = 0;
                 return svfk::sim_known_occupancy(list, dl, bytes, &w) == hipSuccess ? w : -1;
             };
-            const int w_top = occ(true, false, bm_bytes + 64 * 8);
+            const int w_top = occ(true, false, bm_bytes + (size_t)svfk::list_slots(64) * 8);
             int64_t lo = std::min<int64_t>(bound, 64), hi = bound;  // occ(lo) >= w_top
             while (lo < hi) {
                 const int64_t mid = lo + (hi - lo + 1) / 2;
-                if (occ(true, false, bm_bytes + (size_t)mid * 8) >= w_top) lo = mid;
+                if (occ(true, false, bm_bytes + (size_t)svfk::list_slots((int)mid) * 8) >= w_top) lo = mid;
                 else hi = mid - 1;
             }
             cap = lo;
@@ -556,7 +556,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
             if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
             const int w_ring = occ(false, h->d_lds, h->lds_bytes);
             const int w_regs = occ(false, h->d_lds, bm_bytes);
-            const int w_list = occ(true, false, bm_bytes + (size_t)cap * 8);
+            const int w_list = occ(true, false, bm_bytes + (size_t)svfk::list_slots((int)cap) * 8);
             int cus = 0;
             if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess)
                 cus = 0;
@@ -571,7 +571,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
             h->list_known = true;
             h->list_stride = (int32_t)bound;
             h->list_cap = (int32_t)cap;
-            h->lds_list = bm_bytes + (size_t)cap * 8;
+            h->lds_list = bm_bytes + (size_t)svfk::list_slots((int)cap) * 8;
             h->lds_list_full = full_bytes;
             h->ring_used = h->any_stepped;
         }
