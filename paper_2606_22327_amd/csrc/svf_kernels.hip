@@ -933,7 +933,9 @@ struct ListProf {
         // writes the candidate behind itself
         const uint32_t ch = (uint32_t)(s_h - t);
         const uint32_t qn = qc1 + ch;
-        for (int tp = ln;;) {
+        // groups down to the one holding entry max(c-1, 0)
+        const int groups = max((ln - max(c - 1, 0) + 63) >> 6, 1);
+        for (int g = 0, tp = ln; g < groups; ++g, tp -= 64) {
             const int b = max(tp - 64, 0);
             const int j = b + lane;
             const int jj = min(j, max(tp - 1, 0));
@@ -945,8 +947,6 @@ struct ListProf {
             const int pos = j < tp ? (mv ? j + 1 : j) : cap + 1 + lane;
             F[pos] = nw ? te : ff;
             Q[pos] = nw ? qn : (mv ? qq + ch : qq);
-            if (b <= c - 1 || b == 0) break;
-            tp = b;
         }
         if (c == 0) {  // no entry before the candidate
             if (lane == 0) {
@@ -974,7 +974,9 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     const int lane = lane_id();
     const int M = P.M;
     const int n = sg.n;
-    int t = uni(st.t), cursor = uni(st.cursor), seq = uni(st.seq), nadm = uni(st.nfin);
+    // admissions so far: seq0 + nstg (known lengths: every admitted request
+    // is finished at start + o, so no other count is needed)
+    int t = uni(st.t), cursor = uni(st.cursor), seq0 = uni(st.seq);
     int max_fin = uni(st.max_fin), head = uni(st.head_rank), t_f = uni(st.t_f);
     int status = STATUS_RUNNING;
 
@@ -1000,10 +1002,9 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     int rwb = INT32_MIN / 2;
     int4 rw = make_int4(0, 0, 0, 0);
     auto rec_of = [&](int r) -> int4 {
-        if (r < rwb || r >= rwb + 64) {
+        if ((unsigned)(r - rwb) >= 64u) {
             rwb = uni(r & ~63);
-            const int i = rwb + lane;
-            rw = i < n ? sg.rec[i] : make_int4(0, 0, 0, 0);
+            rw = sg.rec[min(rwb + lane, n - 1)];  // lanes past the end: a copy
         }
         return readlane4(rw, r - rwb);
     };
@@ -1013,7 +1014,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     // (request index and start step), and written out 64 at a time with their
     // admission numbers, so that no store is in flight behind each admission;
     // the finish (start + o) is derived when the outputs are finalised.
-    int stg_idx = 0, stg_t = 0, nstg = 0, seq0 = seq;
+    int stg_idx = 0, stg_t = 0, nstg = 0;
     auto flush = [&]() {
         if (lane < nstg) {
             sg.start[stg_idx] = stg_t;
@@ -1037,7 +1038,9 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
 
     for (;;) {
         // every request finished by step t-1 (an empty instance is done at t = 0)
-        if (nadm == n && (nadm == 0 || max_fin <= t - 1)) { status = STATUS_DONE; break; }
+        if (seq0 + nstg == n) {
+            if (n == 0 || max_fin <= t - 1) { status = STATUS_DONE; break; }
+        }
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
         if (t >= t_lim) break;
 
@@ -1093,20 +1096,22 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                     if (cbits == 0ull) S[cw >> 6] &= ~(1ull << (cw & 63));
                 }
                 lds_order();
-                ++seq;
-                ++nadm;
                 max_fin = max(max_fin, t + q.w);
                 // Once every arrival ranked above the old head is running, the
                 // old head (record known) is next, or nothing is left waiting.
                 // Before t_f it still does not fit: the profile has only grown
                 // since t_f was computed, which can only delay the release.
-                if (r < old_head && --n_below == 0) {
-                    if (old_head == INT32_MAX) { head = -1; break; }
-                    if (t < t_f) break;
-                    r = old_head;
-                    q = hq0;
-                    if (cw != (r >> 6)) load_word(r >> 6);
-                    continue;
+                // (Candidates come in rank order, so the first n_below of them
+                // are exactly those arrivals.)
+                if (n_below > 0) {
+                    if (--n_below == 0) {
+                        if (old_head == INT32_MAX) { head = -1; break; }
+                        if (t < t_f) break;
+                        r = old_head;
+                        q = hq0;
+                        if (cw != (r >> 6)) load_word(r >> 6);
+                        continue;
+                    }
                 }
                 if (cbits != 0ull) {
                     r = cw * 64 + __builtin_ctzll(cbits);
@@ -1138,7 +1143,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     flush();
     // the peak over the steps up to t
     const int pk = prof.end(t);
-    st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nadm; st.max_fin = max_fin;
+    st.t = t; st.cursor = cursor; st.seq = seq0; st.nfin = seq0; st.max_fin = max_fin;
     st.head_rank = head; st.t_f = t_f; st.status = status;
     st.peak = max(st.peak, (int64_t)pk);
 }
