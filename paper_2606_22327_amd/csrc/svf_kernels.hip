@@ -1044,15 +1044,17 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
         if (t >= t_lim) break;
 
-        // 1. arrivals: a prefix of the window (arrivals are sorted).  n_below
-        //    counts those ranked above the blocked head (the lowest waiting
-        //    rank before this step; none if nothing was waiting).
+        // 1. arrivals up to t: a prefix of the window (arrivals are sorted;
+        //    those of earlier steps were ranked below the blocked head, so
+        //    nothing could happen at their steps).  n_below counts those
+        //    ranked above the blocked head (the lowest waiting rank before
+        //    this step; none if nothing was waiting).
         const int old_head = head < 0 ? INT32_MAX : head;
         const int4 hq0 = hq;
         int new_min = INT32_MAX, n_below = 0;
         int4 nq = make_int4(0, 0, 0, 0);
         for (;;) {
-            const bool arr = (wb + lane >= cursor) && (a_reg == t);
+            const bool arr = (wb + lane >= cursor) && (a_reg <= t);
             const uint64_t m = ballot(arr);
             if (m == 0ull) break;
             if (arr) bitmap_set_atomic(B, S, rk_reg);
@@ -1127,13 +1129,20 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         // the candidate is the head, checked again at t when the segment resumes
         if (prof.stopped()) break;
 
-        // 5. advance to the next step where anything can happen
-        const int next_arr = cursor < wb + 64 ? __builtin_amdgcn_readlane(a_reg, cursor - wb)
-                                              : (cursor < n ? uni(sg.a[cursor]) : INT32_MAX);
+        // 5. advance to the next step where anything can happen: with a
+        //    blocked head, its release or the next arrival ranked above it
+        //    (past the window: the window's end)
         int nt;
-        if (head >= 0) nt = min(t_f, next_arr);
-        else if (cursor < n) nt = next_arr;
-        else nt = max_fin + 1;
+        if (head >= 0) {
+            const uint64_t up = ballot((wb + lane >= cursor) && rk_reg < head);
+            const int next_up = up != 0ull ? __builtin_amdgcn_readlane(a_reg, __builtin_ctzll(up))
+                                           : (wb + 64 < n ? uni(sg.a[wb + 64]) : INT32_MAX);
+            nt = min(t_f, next_up);
+        } else if (cursor < n) {
+            nt = cursor < wb + 64 ? __builtin_amdgcn_readlane(a_reg, cursor - wb) : uni(sg.a[cursor]);
+        } else {
+            nt = max_fin + 1;
+        }
         nt = max(nt, t + 1);
         nt = min(nt, t_lim);
         nt = min(nt, P.max_steps + 1);
