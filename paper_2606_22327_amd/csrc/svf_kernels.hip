@@ -13,7 +13,7 @@
 //                     (each element finds its output slot by binary search in
 //                     the partner run)
 //   k_build_rec       rank-ordered request records and the index->rank map
-//   k_sim<D_LDS, STEPPED>, k_sim_list
+//   k_sim<D_LDS, STEPPED>, k_sim_list, k_sim_list_resume
 //                     the simulation: one wave64 per segment (profile as a ring,
 //                     per-step or event-driven; or as a finish-ordered list)
 //   k_finalize        per-request outputs as of the reached step (finish derived
@@ -1548,6 +1548,13 @@ void k_sim_list(SimArgs P) {
     sim_segment<false, false, true>(P);
 }
 
+// The same for the continuation of segments whose list outgrew the first
+// launch's LDS (a kernel of its own, so that timings keep the two apart).
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(8, 8)))
+void k_sim_list_resume(SimArgs P) {
+    sim_segment<false, false, true>(P);
+}
+
 // ------------------------------------------------------------ finalize
 
 __global__ __launch_bounds__(64) void k_finalize(FinArgs F) {
@@ -1696,7 +1703,8 @@ hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool li
                       size_t lds_bytes, hipStream_t s) {
     if (G <= 0) return hipSuccess;
     if (!stepped && list) {
-        hipLaunchKernelGGL(k_sim_list, dim3(G), dim3(64), lds_bytes, s, P);
+        if (P.list_resume) hipLaunchKernelGGL(k_sim_list_resume, dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL(k_sim_list, dim3(G), dim3(64), lds_bytes, s, P);
     } else if (d_lds) {
         if (stepped) hipLaunchKernelGGL((k_sim<true, true>), dim3(G), dim3(64), lds_bytes, s, P);
         else hipLaunchKernelGGL((k_sim<true, false>), dim3(G), dim3(64), lds_bytes, s, P);
@@ -1722,6 +1730,7 @@ hipError_t prepare_sim(bool d_lds, size_t lds_ring, bool list, size_t lds_list) 
         if (e == hipSuccess) e = sim_attr((const void*)k_sim<false, false>, lds_ring);
     }
     if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_list, lds_list);
+    if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_list_resume, lds_list);
     return e;
 }
 
