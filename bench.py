@@ -32,9 +32,14 @@ def log(msg):
 
 
 def kernel_source_digest():
+    """Digest of what the kernels are built from: their source and the GPU
+    compiler flags."""
     import hashlib
+    from paper_2606_22327_amd import build as B
+
     src = os.path.join(ROOT, "paper_2606_22327_amd", "csrc", "svf_kernels.hip")
-    return hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    data = open(src, "rb").read() + " ".join(B.GPU_FLAGS).encode()
+    return hashlib.sha256(data).hexdigest()[:16]
 
 
 def traffic_from_profile(workload):

@@ -18,8 +18,11 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsvfsim.so")
 
 ARCH = os.environ.get("SVFSIM_ARCH", "gfx950")
-# Packed FP32 instructions are kept out of every code object.
-GPU_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Packed FP32 instructions are kept out of every code object.  Uniform
+# branches are left as scalar branches rather than structured with lane masks
+# (the simulation kernels are bound by scalar instruction issue).
+GPU_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-mllvm", "-structurizecfg-skip-uniform-regions"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
 
 
