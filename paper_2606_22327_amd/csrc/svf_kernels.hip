@@ -933,20 +933,27 @@ struct ListProf {
         // writes the candidate behind itself
         const uint32_t ch = (uint32_t)(s_h - t);
         const uint32_t qn = qc1 + ch;
-        // groups down to the one holding entry max(c-1, 0)
-        const int groups = max((ln - max(c - 1, 0) + 63) >> 6, 1);
-        for (int g = 0, tp = ln; g < groups; ++g, tp -= 64) {
-            const int b = max(tp - 64, 0);
+        auto shift = [&](int b, int tp, int ff, uint32_t qq) {
             const int j = b + lane;
-            const int jj = min(j, max(tp - 1, 0));
-            const int ff = F[jj];
-            const uint32_t qq = Q[jj];
             const bool mv = j >= c - 1;
             const bool nw = j == c - 1;
             // lanes past the group's end: a slot of their own behind the capacity
             const int pos = j < tp ? (mv ? j + 1 : j) : cap + 1 + lane;
             F[pos] = nw ? te : ff;
             Q[pos] = nw ? qn : (mv ? qq + ch : qq);
+        };
+        if (top == ln) {
+            // the check read only the last group, which holds entry c-1 (or
+            // is the first group): shift it from the registers
+            shift(base, top, f, q);
+        } else {
+            // groups down to the one holding entry max(c-1, 0)
+            const int groups = max((ln - max(c - 1, 0) + 63) >> 6, 1);
+            for (int g = 0, tp = ln; g < groups; ++g, tp -= 64) {
+                const int b = max(tp - 64, 0);
+                const int jj = min(b + lane, max(tp - 1, 0));
+                shift(b, tp, F[jj], Q[jj]);
+            }
         }
         if (c == 0) {  // no entry before the candidate
             if (lane == 0) {
