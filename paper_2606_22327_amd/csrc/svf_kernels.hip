@@ -911,14 +911,19 @@ struct ListProf {
             // the release step: max over the violating steps of min(tau, D + tau - X),
             // over the same groups again (base: the lowest one scanned)
             int rel = min(te, ve - X);
-            for (int tp = ln;;) {
-                const int b = max(tp - 64, 0);
-                const int jj = min(b + lane, tp - 1);
-                const int ff = F[jj];
-                const int v = (int)(Q[jj] + (uint32_t)ff * (uint32_t)(jj + 2));
-                rel = max(rel, ff <= te ? min(ff, v - X) : INT32_MIN);
-                if (b <= base) break;
-                tp = b;
+            if (top == ln) {  // one group, still in the registers
+                const int v = (int)(q + (uint32_t)f * (uint32_t)(jr + 2));
+                rel = max(rel, f <= te ? min(f, v - X) : INT32_MIN);
+            } else {
+                for (int tp = ln;;) {
+                    const int b = max(tp - 64, 0);
+                    const int jj = min(b + lane, tp - 1);
+                    const int ff = F[jj];
+                    const int v = (int)(Q[jj] + (uint32_t)ff * (uint32_t)(jj + 2));
+                    rel = max(rel, ff <= te ? min(ff, v - X) : INT32_MIN);
+                    if (b <= base) break;
+                    tp = b;
+                }
             }
             *t_free = wmax(rel);
             return false;
