@@ -13,7 +13,7 @@
 //                     (each element finds its output slot by binary search in
 //                     the partner run)
 //   k_build_rec       rank-ordered request records and the index->rank map
-//   k_sim<D_LDS, STEPPED>, k_sim_list, k_sim_list_resume
+//   k_sim<D_LDS, STEPPED>, k_sim_list, k_sim_list_resume, k_sim_steplist
 //                     the simulation: one wave64 per segment (profile as a ring,
 //                     per-step or event-driven; or as a finish-ordered list)
 //   k_finalize        per-request outputs as of the reached step (finish derived
@@ -1171,6 +1171,216 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
 
 // ---- planned lengths differ from the truth: one step at a time
 
+// The per-step path keeps the planned memory of the requests that are still
+// within their planned length (each started at k with planned length L holds
+// s + tau - k at the steps tau in [k+1, k+L]) in one of two forms: the ring
+// (RingStep) or the finish-ordered list (StepList).  Both offer begin (at
+// step t, before anything reads the profile: requests whose planned length
+// ends by t leave it), next (their memory at step t+1), fit (the check of a
+// candidate over the steps t+1 .. t+min(oh, chk), with extra1 added at t+1,
+// and its admission for its whole planned length; *t_free as in
+// fit_and_admit), remove (a request's planned memory after t) and end_step.
+template <bool LDS>
+struct RingStep {
+    const Ring<LDS>& D;
+    __device__ __forceinline__ explicit RingStep(const Ring<LDS>& d) : D(d) {}
+    __device__ __forceinline__ void begin(int) {}
+    __device__ __forceinline__ int64_t next(int t) const { return (int64_t)D.ld(t + 1) - (t + 1); }
+    __device__ __forceinline__ bool fit(int t, int s_h, int oh, int M, int extra1, int maxF,
+                                        int* t_free, int chk) {
+        return fit_and_admit(D, t, s_h, oh, M, extra1, maxF, t_free, chk);
+    }
+    __device__ __forceinline__ void remove(int t, int s, int k, int L) { remove_future(D, t, s, k, L); }
+    __device__ __forceinline__ void end_step(int t) {
+        // the slot of step t+1 becomes the one of step t+1+H (nothing planned yet)
+        Ring<LDS>::order();
+        if (lane_id() == 0) D.st(t + 1, t + 1 + D.H);
+        Ring<LDS>::order();
+    }
+};
+
+// The list of the event path, with what the per-step path needs besides:
+// entries leave at their planned finish (the request then either completes
+// or runs on past its plan, which the caller accounts for), an entry can be
+// removed from the middle (early completion, eviction), the check may stop
+// short of the candidate's planned finish (next-step admission) and carries
+// the memory of the requests past their plan at t+1.  Its capacity is the
+// host's bound on concurrent requests, so it is never full.
+struct StepList {
+    int32_t* F;     // [list_slots(cap)] planned finish, descending
+    uint32_t* Q;    // [list_slots(cap)] prefix sums of s - k
+    int cap;
+    int ln;
+    uint32_t tot;
+    struct Scan {
+        int m, base, top, f, jr, c;
+        uint32_t q, qc1;
+    };
+    // Groups of 64 from the end down to the one holding an entry with F > tx
+    // (or the first): m = the lanes' largest D(F_j) + F_j over F_j <= tx, c =
+    // #{F >= tx}, qc1 = Q_{c-1} (0 if c = 0).
+    __device__ __forceinline__ Scan scan_to(int tx) const {
+        const int lane = lane_id();
+        Scan r;
+        r.m = INT32_MIN;
+        r.top = ln;
+        for (;;) {
+            r.base = max(r.top - 64, 0);
+            r.jr = min(r.base + lane, max(r.top - 1, 0));
+            r.f = F[r.jr];
+            r.q = Q[r.jr];
+            r.m = max(r.m, r.f <= tx ? (int)(r.q + (uint32_t)r.f * (uint32_t)(r.jr + 2)) : INT32_MIN);
+            if (r.base == 0) break;
+            if (__builtin_amdgcn_readfirstlane(r.f) > tx) break;
+            r.top = r.base;
+        }
+        const int ge = min((int)__popcll(ballot(r.f >= tx)), r.top - r.base);
+        r.c = r.base + ge;
+        r.qc1 = ge > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)r.q, ge - 1) : 0u;
+        return r;
+    }
+    __device__ __forceinline__ void begin(int t) {
+        const int lane = lane_id();
+        if (ln == 0 || __builtin_amdgcn_readfirstlane(F[ln - 1]) > t) return;
+        while (ln > 0) {
+            const int top = ln, base = max(top - 64, 0);
+            const int jr = min(base + lane, top - 1);
+            const uint64_t dm = ballot(F[jr] <= t);
+            if (dm == 0ull) break;
+            const uint32_t q = Q[jr];
+            ln = top - ((int)__popcll(dm) - (64 - (top - base)));
+            if (ln > base) {
+                tot = (uint32_t)__builtin_amdgcn_readlane((int)q, ln - 1 - base);
+                break;
+            }
+            if (ln == 0) {
+                tot = 0u;
+                if (lane == 0) F[0] = INT32_MAX;  // an empty list reads as "finishes last"
+                lds_order();
+            }
+        }
+    }
+    // all entries have F >= t+1 (begin(t) ran)
+    __device__ __forceinline__ int64_t next(int t) const {
+        return (int64_t)(int)(tot + (uint32_t)ln * (uint32_t)(t + 1));
+    }
+    __device__ __forceinline__ bool fit(int t, int s_h, int oh, int M, int extra1, int maxF,
+                                        int* t_free, int chk) {
+        (void)maxF;
+        const int lane = lane_id();
+        const int te = t + oh;
+        const int tc = t + min(oh, chk);  // the last step checked
+        const int X = M - s_h;
+        const int lim = X + t;
+        // step t+1 with the memory of the requests past their plan
+        const int v1 = (int)(tot + (uint32_t)(ln + 1) * (uint32_t)(t + 1)) + extra1;
+        Scan a = scan_to(tc);
+        const int vc = (int)(a.qc1 + (uint32_t)tc * (uint32_t)(a.c + 1));
+        if (ballot(max(a.m, max(vc, v1)) > lim) != 0ull) {
+            // the release step: max over the violating steps of min(tau, D + tau - X)
+            int rel = max(min(tc, vc - X), min(t + 1, v1 - X));
+            if (a.top == ln) {
+                const int v = (int)(a.q + (uint32_t)a.f * (uint32_t)(a.jr + 2));
+                rel = max(rel, a.f <= tc ? min(a.f, v - X) : INT32_MIN);
+            } else {
+                for (int tp = ln;;) {
+                    const int b = max(tp - 64, 0);
+                    const int jj = min(b + lane, tp - 1);
+                    const int ff = F[jj];
+                    const int v = (int)(Q[jj] + (uint32_t)ff * (uint32_t)(jj + 2));
+                    rel = max(rel, ff <= tc ? min(ff, v - X) : INT32_MIN);
+                    if (b <= a.base) break;
+                    tp = b;
+                }
+            }
+            *t_free = wmax(rel);
+            return false;
+        }
+        if (ln >= cap) {  // only if the host's bound were wrong
+            *t_free = INT32_MAX;
+            return false;
+        }
+        // the candidate goes in at its planned finish te
+        if (tc != te) a = scan_to(te);
+        const int c = a.c;
+        const uint32_t ch = (uint32_t)(s_h - t);
+        const uint32_t qn = a.qc1 + ch;
+        auto shift = [&](int b, int tp, int ff, uint32_t qq) {
+            const int j = b + lane;
+            const bool mv = j >= c - 1;
+            const bool nw = j == c - 1;
+            const int pos = j < tp ? (mv ? j + 1 : j) : cap + 1 + lane;
+            F[pos] = nw ? te : ff;
+            Q[pos] = nw ? qn : (mv ? qq + ch : qq);
+        };
+        if (a.top == ln) {
+            shift(a.base, a.top, a.f, a.q);
+        } else {
+            const int groups = max((ln - max(c - 1, 0) + 63) >> 6, 1);
+            for (int g = 0, tp = ln; g < groups; ++g, tp -= 64) {
+                const int b = max(tp - 64, 0);
+                const int jj = min(b + lane, max(tp - 1, 0));
+                shift(b, tp, F[jj], Q[jj]);
+            }
+        }
+        if (c == 0) {
+            if (lane == 0) {
+                F[0] = te;
+                Q[0] = qn;
+            }
+        }
+        lds_order();
+        ++ln;
+        tot += ch;
+        return true;
+    }
+    // Remove the entry of a request started at k with planned length L
+    // (planned finish k + L > t); entries with equal F and s - k are
+    // interchangeable.
+    __device__ __forceinline__ void remove(int t, int s, int k, int L) {
+        (void)t;
+        const int lane = lane_id();
+        const int fd = k + L;
+        const uint32_t cd = (uint32_t)(s - k);
+        // find it: groups from the end (its F is at least that of the last entry)
+        int p = -1;
+        for (int top = ln; top > 0;) {
+            const int base = max(top - 64, 0);
+            const int j = base + lane;
+            const int jr = min(j, top - 1);
+            const int f = F[jr];
+            const uint32_t qp = jr > 0 ? Q[jr - 1] : 0u;
+            const uint64_t hit = ballot(j < top && f == fd && Q[jr] - qp == cd);
+            if (hit != 0ull) {
+                p = base + (int)__builtin_ctzll(hit);
+                break;
+            }
+            if (base == 0 || __builtin_amdgcn_readfirstlane(f) > fd) break;
+            top = base;
+        }
+        if (p < 0) return;  // not in the list (cannot happen)
+        // entries p+1 .. ln-1 move down by one and lose s - k
+        for (int b = p; b < ln; b += 64) {
+            const int j = b + lane;
+            const int jr = min(j, ln - 1);
+            const int f = F[jr];
+            const uint32_t q = Q[jr];
+            const int pos = (j > p && j < ln) ? j - 1 : cap + 1 + lane;
+            F[pos] = f;
+            Q[pos] = q - cd;
+        }
+        lds_order();
+        --ln;
+        tot -= cd;
+        if (ln == 0) {
+            if (lane == 0) F[0] = INT32_MAX;
+            lds_order();
+        }
+    }
+    __device__ __forceinline__ void end_step(int) {}
+};
+
+
 // The running list (global memory, small enough to stay in L2): entry x
 // holds the record {index, s, planned length, true length} of a running
 // request and {start step, rank}.
@@ -1181,9 +1391,9 @@ struct RunList {
     __device__ __forceinline__ static void order() { __syncthreads(); }
 };
 
-template <bool LDS>
+template <class PROF>
 __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
-                            const Ring<LDS>& D, const RunList& A, SegState& st, int t_lim) {
+                            PROF& D, const RunList& A, SegState& st, int t_lim) {
     const int lane = lane_id();
     const int M = P.M;
     const int n = sg.n;
@@ -1197,7 +1407,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     const int pol = blockIdx.x / P.I;
     const int chk = (P.policies[pol] & ADMIT_CURRENT) ? 1 : (1 << 30);
     // memory planned for step t+1 by requests within their planned length
-    auto planned_next = [&]() -> int64_t { return (int64_t)D.ld(t + 1) - (t + 1); };
+    auto planned_next = [&]() -> int64_t { return D.next(t); };
 
     // arrival window: lane l holds the arrival and rank of request wb + l
     int wb = 0, a_reg = INT32_MAX, rk_reg = 0;
@@ -1301,9 +1511,8 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                     while (early) {
                         const int src = __builtin_ctzll(early);
                         early &= early - 1;
-                        remove_future(D, t, __builtin_amdgcn_readlane(s, src),
-                                      __builtin_amdgcn_readlane(k, src),
-                                      __builtin_amdgcn_readlane(oh, src));
+                        D.remove(t, __builtin_amdgcn_readlane(s, src), __builtin_amdgcn_readlane(k, src),
+                                 __builtin_amdgcn_readlane(oh, src));
                     }
                     const uint64_t keep = ballot(live && !done);
                     dfin += __popcll(dm);
@@ -1323,6 +1532,8 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             next_ev = wmin(nxt);
             RunList::order();  // the compacted list is read again below
         }
+        // requests whose planned length ends by t leave the planned profile
+        D.begin(t);
         // 3. overflow of the true memory at t+1: evict the largest believed
         //    remaining volume (latest arrival on ties)
         int nev = 0;
@@ -1363,7 +1574,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                 const int2 vkr = A.kr[vpos];
                 const int k = vkr.x;
                 const int e = t - k;
-                if (e < q.z) remove_future(D, t, q.y, k, q.z);
+                if (e < q.z) D.remove(t, q.y, k, q.z);
                 else { C_O -= (int64_t)(q.y - k); N_O -= 1; }
                 if (lane == 0) {
                     A.q[vpos] = A.q[nA - 1];
@@ -1389,7 +1600,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             int tf = 0;
             // memory of requests past their plan at t+1; <= M after step 3
             const int extra1 = (int)(C_O + (int64_t)N_O * (t + 1));
-            if (!fit_and_admit(D, t, q.y, q.z, M, extra1, maxF, &tf, chk)) {
+            if (!D.fit(t, q.y, q.z, M, extra1, maxF, &tf, chk)) {
                 blk = r;
                 // If the next step alone is over (true memory at t+1 plus the
                 // candidate's first token), the candidate stays blocked until
@@ -1427,9 +1638,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         req_steps += nA;
         const int64_t mem = planned_next() + C_O + (int64_t)N_O * (t + 1);
         peak = max(peak, mem);
-        Ring<LDS>::order();
-        if (lane == 0) D.st(t + 1, t + 1 + D.H);
-        Ring<LDS>::order();
+        D.end_step(t);
         ++t;
     }
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nfin; st.nA = nA; st.N_O = N_O;
@@ -1482,7 +1691,35 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
     const int64_t want = (int64_t)st.t + P.step_delta;
     int t_lim = (int)min(want, (int64_t)P.max_steps + 2);
 
-    if (LIST) {
+    if (LIST && STEPPED) {
+        // the per-step path's list has room for the host's bound
+        const int cap = P.list_stride;
+        int32_t* Fg = P.lst_f + (int64_t)g * P.list_stride;
+        uint32_t* Qg = P.lst_q + (int64_t)g * P.list_stride;
+        StepList L;
+        L.cap = cap;
+        L.F = reinterpret_cast<int32_t*>(smem + P.bw_max);
+        L.Q = reinterpret_cast<uint32_t*>(L.F + list_slots(cap));
+        L.ln = uni(st.ln);
+        L.tot = (uint32_t)uni((int)st.lq);
+        for (int x = lane; x < L.ln; x += 64) {
+            L.F[x] = Fg[x];
+            L.Q[x] = Qg[x];
+        }
+        if (L.ln == 0 && lane == 0) L.F[0] = INT32_MAX;  // the empty list's sentinel
+        __syncthreads();
+        RunList A;
+        A.q = sg.act;
+        A.kr = sg.actkr;
+        run_stepped(P, sg, B, S, W1, L, A, st, t_lim);
+        __syncthreads();
+        for (int x = lane; x < L.ln; x += 64) {
+            Fg[x] = L.F[x];
+            Qg[x] = L.Q[x];
+        }
+        st.ln = L.ln;
+        st.lq = L.tot;
+    } else if (LIST) {
         const int cap = P.list_cap;
         int32_t* Fg = P.lst_f + (int64_t)g * P.list_stride;
         uint32_t* Qg = P.lst_q + (int64_t)g * P.list_stride;
@@ -1533,7 +1770,8 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
             RunList A;
             A.q = sg.act;
             A.kr = sg.actkr;
-            run_stepped(P, sg, B, S, W1, D, A, st, t_lim);
+            RingStep<D_LDS> R(D);
+            run_stepped(P, sg, B, S, W1, R, A, st, t_lim);
         } else {
             RingProf<D_LDS> R(D, uni(st.t));
             run_known(P, sg, B, S, W1, R, st, t_lim);
@@ -1558,6 +1796,11 @@ __global__ __launch_bounds__(64) void k_sim(SimArgs P) {
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(8, 8)))
 void k_sim_list(SimArgs P) {
     sim_segment<false, false, true>(P);
+}
+
+// The per-step path with the finish-ordered list.
+__global__ __launch_bounds__(64) void k_sim_steplist(SimArgs P) {
+    sim_segment<false, true, true>(P);
 }
 
 // The same for the continuation of segments whose list outgrew the first
@@ -1714,7 +1957,9 @@ hipError_t launch_sort_rec(const SortArgs& A, int G, int max_n, hipStream_t s) {
 hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool list,
                       size_t lds_bytes, hipStream_t s) {
     if (G <= 0) return hipSuccess;
-    if (!stepped && list) {
+    if (stepped && list) {
+        hipLaunchKernelGGL(k_sim_steplist, dim3(G), dim3(64), lds_bytes, s, P);
+    } else if (!stepped && list) {
         if (P.list_resume) hipLaunchKernelGGL(k_sim_list_resume, dim3(G), dim3(64), lds_bytes, s, P);
         else hipLaunchKernelGGL(k_sim_list, dim3(G), dim3(64), lds_bytes, s, P);
     } else if (d_lds) {
@@ -1742,6 +1987,7 @@ hipError_t prepare_sim(bool d_lds, size_t lds_ring, bool list, size_t lds_list) 
         if (e == hipSuccess) e = sim_attr((const void*)k_sim<false, false>, lds_ring);
     }
     if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_list, lds_list);
+    if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_steplist, lds_list);
     if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_list_resume, lds_list);
     return e;
 }

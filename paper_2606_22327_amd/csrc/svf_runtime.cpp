@@ -67,6 +67,8 @@ struct svf_batch {
     int32_t list_cap = 0;     // list entries per segment in LDS (first launch)
     size_t lds_list = 0;      // LDS of the event kernel with the list
     size_t lds_list_full = 0; //   and with room for the bound (continuation)
+    bool list_stepped = false; // per-step path: profile as the finish-ordered list
+    size_t lds_step = 0;       // LDS of the per-step kernel with the list
     int32_t kbits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t bw_total = 0;
     bool d_lds = true;
@@ -393,7 +395,8 @@ int do_sim(svf_batch* h, int64_t delta) {
         }
     }
     if (h->n_stepped > 0)
-        HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, false, h->lds_bytes, h->stream));
+        HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, h->list_stepped,
+                                h->list_stepped ? h->lds_step : h->lds_bytes, h->stream));
     record_end(h, 1, e0);
     h->sim_launches += 1;
     h->dirty = true;
@@ -533,9 +536,10 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     // the largest capacity that still lets as many waves reside as the list
     // kernel's registers allow; segments that outgrow it stop, and a second
     // launch with room for the bound on concurrent requests continues them.
+    const int64_t bound = (h->n_known > 0 || h->any_stepped)
+                              ? std::max<int64_t>(1, running_bound(v.s, off, d->M)) : 1;
+    const size_t full_bytes = bm_bytes + (size_t)svfk::list_slots((int)std::min<int64_t>(bound, 1 << 24)) * 8;
     if (h->n_known > 0) {
-        const int64_t bound = std::max<int64_t>(1, running_bound(v.s, off, d->M));
-        const size_t full_bytes = bm_bytes + (size_t)svfk::list_slots((int)bound) * 8;
         const char* pe = getenv("SVFSIM_PROFILE");
         bool use = false;
         int64_t cap = bound;
@@ -569,13 +573,25 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
         if (pe && !strcmp(pe, "list")) use = full_bytes <= 160 * 1024;
         if (use) {
             h->list_known = true;
-            h->list_stride = (int32_t)bound;
             h->list_cap = (int32_t)cap;
             h->lds_list = bm_bytes + (size_t)svfk::list_slots((int)cap) * 8;
             h->lds_list_full = full_bytes;
-            h->ring_used = h->any_stepped;
         }
     }
+    // The per-step path keeps its planned profile as the finish-ordered list
+    // (room for the bound, no continuation) when that fits in 64 KB of LDS.
+    if (h->any_stepped) {
+        const char* ps = getenv("SVFSIM_STEP_PROFILE");
+        bool use = full_bytes <= 64 * 1024;
+        if (ps && !strcmp(ps, "ring")) use = false;
+        if (ps && !strcmp(ps, "list")) use = full_bytes <= 160 * 1024;
+        if (use) {
+            h->list_stepped = true;
+            h->lds_step = full_bytes;
+        }
+    }
+    if (h->list_known || h->list_stepped) h->list_stride = (int32_t)bound;
+    h->ring_used = (h->n_known > 0 && !h->list_known) || (h->any_stepped && !h->list_stepped);
     if (h->lds_bytes > 160 * 1024) {
         delete h;
         return fail(SVF_EINVAL, "an instance's rank bitmap needs %zu bytes of LDS (> 160 KB)", h->lds_bytes);
@@ -605,7 +621,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     ALLOC(d_bw_off, I + 1);
     ALLOC(d_bitmap, (int64_t)P * h->bw_total);
     if (h->ring_used) ALLOC(d_ring, G * (h->H + 64));
-    if (h->list_known) {
+    if (h->list_known || h->list_stepped) {
         ALLOC(d_lst_f, G * (int64_t)h->list_stride);
         ALLOC(d_lst_q, G * (int64_t)h->list_stride);
     }
@@ -645,7 +661,8 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
 #undef CPY
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess) {
-        hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes, h->list_known, h->lds_list_full);
+        hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes, h->list_known || h->list_stepped,
+                                         std::max(h->lds_list_full, h->lds_step));
         if (a != hipSuccess) e = a;
     }
     if (e == hipSuccess && h->fused_sort) {

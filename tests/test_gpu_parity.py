@@ -345,6 +345,38 @@ def test_event_path_both_profiles(profile):
         os.environ.pop("SVFSIM_LIST_LDS_CAP", None)
 
 
+@pytest.mark.parametrize("profile", ["ring", "list"])
+def test_stepped_path_both_profiles(profile):
+    """The per-step path (1-bit SVF, predicted lengths, next-step admission)
+    keeps the planned profile either in the ring or in the finish-ordered
+    list (early completions and evictions remove entries from its middle).
+    Each forced on the same batches, against the oracle, also step by step."""
+    os.environ["SVFSIM_STEP_PROFILE"] = profile
+    try:
+        b3 = W.config(3, instances=24, n=600)
+        say(f"step profile {profile}: config 3 reduced")
+        g3 = gpu_run(b3)
+        for pol in b3.policies:
+            compare(b3, g3[pol], pol, label=f"{profile}-cfg3")
+        assert int(g3["svf1bit"]["stats"]["preemptions"].sum()) > 0
+        b4 = W.with_predictor(W.config(4, instances=3, n=2000, policies=("svf", "svf+cur")), 0.5)
+        say(f"step profile {profile}: config 4 reduced, predicted lengths, chunked")
+        g4 = gpu_run(b4, chunks=[53, 1, 700, 3, 2500, 1 << 20])
+        for pol in b4.policies:
+            compare(b4, g4[pol], pol, label=f"{profile}-pred-cfg4")
+        for seed in range(3):
+            r = W.random_small(300 + seed, instances=40, n_max=80, s_max=12, o_max=30, M=70,
+                               gap_mean=[0.0, 0.3, 1.0][seed], bits=seed == 0,
+                               plan_noise=seed != 0)
+            r.policies = ("svf", "svf+cur", "sjf+cur") if seed else ("svf1bit", "svf1bit+cur")
+            r.max_steps = W.default_max_steps(r)
+            gr = gpu_run(r)
+            for pol in r.policies:
+                compare(r, gr[pol], pol, label=f"{profile}-random{seed}")
+    finally:
+        del os.environ["SVFSIM_STEP_PROFILE"]
+
+
 def test_degenerate_cases():
     say("degenerate cases")
     # all instances empty
