@@ -1600,14 +1600,20 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             int tf = 0;
             // memory of requests past their plan at t+1; <= M after step 3
             const int extra1 = (int)(C_O + (int64_t)N_O * (t + 1));
+            // If the next step alone is over (true memory at t+1 plus the
+            // candidate's first token), the candidate fails the check and
+            // stays blocked until something is released: without completions
+            // or evictions the running set only grows, by one token per
+            // request per step.
+            if (planned_next() + extra1 + q.y + 1 > M) {
+                blk = r;
+                blk_tf = INT32_MAX;
+                relaxed = false;
+                break;
+            }
             if (!D.fit(t, q.y, q.z, M, extra1, maxF, &tf, chk)) {
                 blk = r;
-                // If the next step alone is over (true memory at t+1 plus the
-                // candidate's first token), the candidate stays blocked until
-                // something is released: without completions or evictions the
-                // running set only grows, by one token per request per step.
-                const bool over1 = planned_next() + extra1 + q.y + 1 > M;
-                blk_tf = over1 ? INT32_MAX : tf;
+                blk_tf = tf;
                 relaxed = false;
                 break;
             }
