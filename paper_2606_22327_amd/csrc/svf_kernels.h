@@ -29,7 +29,8 @@ struct SegState {
     int32_t ln;         // event path with the list profile: running requests
     uint32_t lq;        //   and the prefix sum of (s - k) of the last entry
     int32_t resume_lim; // list full before step resume_lim: continue up to there (0: no)
-    int32_t pad;
+    int32_t resume_nev; // per-step path: -1, or stopped in the admission phase of step t
+                        //   with this many evictions of that step (ranks in evl)
 };
 
 // Same layout as svf_instance_stats of the public header.
@@ -136,6 +137,8 @@ hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool li
                       size_t lds_bytes, hipStream_t s);
 // resident waves per compute unit of the event kernel (ring or list profile)
 hipError_t sim_known_occupancy(bool list, bool d_lds, size_t lds_bytes, int* blocks);
+// resident waves per compute unit of the per-step kernel with the list
+hipError_t sim_step_occupancy(size_t lds_bytes, int* blocks);
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s);
 
 }  // namespace svfk

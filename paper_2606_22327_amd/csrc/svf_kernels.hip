@@ -13,7 +13,8 @@
 //                     (each element finds its output slot by binary search in
 //                     the partner run)
 //   k_build_rec       rank-ordered request records and the index->rank map
-//   k_sim<D_LDS, STEPPED>, k_sim_list, k_sim_list_resume, k_sim_steplist
+//   k_sim<D_LDS, STEPPED>, k_sim_list, k_sim_list_resume, k_sim_steplist,
+//   k_sim_steplist_stop, k_sim_steplist_resume
 //                     the simulation: one wave64 per segment (profile as a ring,
 //                     per-step or event-driven; or as a finish-ordered list)
 //   k_finalize        per-request outputs as of the reached step (finish derived
@@ -140,7 +141,7 @@ __global__ void k_init_state(SegState* __restrict__ st, int32_t G) {
     z.t = 0; z.cursor = 0; z.seq = 0; z.status = STATUS_RUNNING;
     z.nA = 0; z.nfin = 0; z.max_fin = 0; z.head_rank = -1;
     z.t_f = 0; z.N_O = 0; z.C_O = 0; z.peak = 0; z.req_steps = 0; z.ln = 0; z.lq = 0;
-    z.resume_lim = 0; z.pad = 0;
+    z.resume_lim = 0; z.resume_nev = -1;
     st[g] = z;
 }
 
@@ -1204,8 +1205,11 @@ struct RingStep {
 // or runs on past its plan, which the caller accounts for), an entry can be
 // removed from the middle (early completion, eviction), the check may stop
 // short of the candidate's planned finish (next-step admission) and carries
-// the memory of the requests past their plan at t+1.  Its capacity is the
-// host's bound on concurrent requests, so it is never full.
+// the memory of the requests past their plan at t+1.  As on the event path,
+// the LDS may hold fewer entries than the host's bound: a candidate that fits
+// into a full list gets *t_free = -1 (a real failure always gives a step
+// after t), which stops the segment inside the admission phase of its step;
+// a launch with room for the bound resumes it there.
 struct StepList {
     int32_t* F;     // [list_slots(cap)] planned finish, descending
     uint32_t* Q;    // [list_slots(cap)] prefix sums of s - k
@@ -1296,8 +1300,8 @@ struct StepList {
             *t_free = wmax(rel);
             return false;
         }
-        if (ln >= cap) {  // only if the host's bound were wrong
-            *t_free = INT32_MAX;
+        if (ln >= cap) {
+            *t_free = -1;
             return false;
         }
         // the candidate goes in at its planned finish te
@@ -1391,7 +1395,9 @@ struct RunList {
     __device__ __forceinline__ static void order() { __syncthreads(); }
 };
 
-template <class PROF>
+// STOP: the profile may fill up (a list with less room than the host's
+// bound); the segment then leaves the launch inside the step.
+template <bool STOP, class PROF>
 __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S, int W1,
                             PROF& D, const RunList& A, SegState& st, int t_lim) {
     const int lane = lane_id();
@@ -1630,6 +1636,10 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             ++seq;
             ++nA;
         }
+        if (STOP && blk_tf < 0) {  // a full list: leave the launch inside this step
+            st.resume_nev = nev;
+            break;
+        }
         // evicted requests compete again from the next step
         if (nev > 0) {
             __syncthreads();  // their ranks were stored by lane 0
@@ -1652,12 +1662,63 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     st.max_fin = maxF;
 }
 
+// The rest of step st.t for a segment that stopped inside its admissions
+// (its steps 1-3 ran in the launch before, evicting nev requests whose ranks
+// are in evl): the admissions with room for the host's bound, the evicted
+// requests back into the waiting set, and the advance to the next step.
+template <class PROF>
+__device__ void stepped_resume_tail(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t* S,
+                                    int W1, PROF& D, const RunList& A, SegState& st, int nev) {
+    const int lane = lane_id();
+    const int M = P.M;
+    const int t = uni(st.t);
+    int seq = uni(st.seq), nA = uni(st.nA), maxF = uni(st.max_fin);
+    const int64_t C_O = st.C_O;
+    const int N_O = st.N_O;
+    const int pol = blockIdx.x / P.I;
+    const int chk = (P.policies[pol] & ADMIT_CURRENT) ? 1 : (1 << 30);
+    const int extra1 = (int)(C_O + (int64_t)N_O * (t + 1));
+    for (;;) {
+        const int r = bitmap_first(B, S, W1);
+        if (r < 0) break;
+        const int4 q = sg.rec[r];
+        if (D.next(t) + extra1 + q.y + 1 > M) break;
+        int tf = 0;
+        if (!D.fit(t, q.y, q.z, M, extra1, maxF, &tf, chk)) break;
+        maxF = max(maxF, t + q.z);
+        if (lane == 0) {
+            bitmap_clear(B, S, r);
+            sg.start[q.x] = t;
+            sg.admit_seq[q.x] = seq;
+            A.q[nA] = q;
+            A.kr[nA] = make_int2(t, r);
+        }
+        RunList::order();
+        ++seq;
+        ++nA;
+    }
+    if (nev > 0) {
+        for (int x = lane; x < nev; x += 64) {
+            const int r = sg.evl[x];
+            if ((unsigned)r < (unsigned)sg.n) bitmap_set_atomic(B, S, r);
+        }
+        lds_order();
+    }
+    st.req_steps += nA;
+    st.peak = max(st.peak, D.next(t) + C_O + (int64_t)N_O * (t + 1));
+    D.end_step(t);
+    st.t = t + 1;
+    st.seq = seq;
+    st.nA = nA;
+    st.max_fin = maxF;
+}
+
 // One wave64 per segment; launched once for segments that plan with the
 // true lengths (event-driven) and once for the others (per step), so each
 // kernel carries only its own path.  LIST: the event path keeps its profile
 // as the finish-ordered list (LDS after the bitmap, kept in global memory
 // between launches) instead of the ring.
-template <bool D_LDS, bool STEPPED, bool LIST>
+template <bool D_LDS, bool STEPPED, bool LIST, bool RESUME = false, bool STOP = false>
 __device__ __forceinline__ void sim_segment(const SimArgs& P) {
     extern __shared__ uint64_t smem[];
     const int g = blockIdx.x;
@@ -1698,8 +1759,7 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
     int t_lim = (int)min(want, (int64_t)P.max_steps + 2);
 
     if (LIST && STEPPED) {
-        // the per-step path's list has room for the host's bound
-        const int cap = P.list_stride;
+        const int cap = P.list_cap;
         int32_t* Fg = P.lst_f + (int64_t)g * P.list_stride;
         uint32_t* Qg = P.lst_q + (int64_t)g * P.list_stride;
         StepList L;
@@ -1708,23 +1768,38 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
         L.Q = reinterpret_cast<uint32_t*>(L.F + list_slots(cap));
         L.ln = uni(st.ln);
         L.tot = (uint32_t)uni((int)st.lq);
-        for (int x = lane; x < L.ln; x += 64) {
-            L.F[x] = Fg[x];
-            L.Q[x] = Qg[x];
+        // resumed inside a step (>= 0), or from the start of one (-1)
+        const int mid = RESUME ? uni(st.resume_nev) : -1;
+        if (RESUME) t_lim = st.resume_lim;
+        st.resume_lim = 0;
+        st.resume_nev = -1;
+        if (L.ln > cap) {
+            // more planned requests than this launch has room for
+            st.resume_lim = t_lim;
+        } else {
+            for (int x = lane; x < L.ln; x += 64) {
+                L.F[x] = Fg[x];
+                L.Q[x] = Qg[x];
+            }
+            if (L.ln == 0 && lane == 0) L.F[0] = INT32_MAX;  // the empty list's sentinel
+            __syncthreads();
+            RunList A;
+            A.q = sg.act;
+            A.kr = sg.actkr;
+            if (RESUME && mid >= 0) {
+                __syncthreads();  // the evicted ranks were stored by lane 0
+                stepped_resume_tail(P, sg, B, S, W1, L, A, st, mid);
+            }
+            run_stepped<STOP>(P, sg, B, S, W1, L, A, st, t_lim);
+            __syncthreads();
+            for (int x = lane; x < L.ln; x += 64) {
+                Fg[x] = L.F[x];
+                Qg[x] = L.Q[x];
+            }
+            st.ln = L.ln;
+            st.lq = L.tot;
+            if (st.resume_nev >= 0) st.resume_lim = t_lim;  // stopped inside step st.t
         }
-        if (L.ln == 0 && lane == 0) L.F[0] = INT32_MAX;  // the empty list's sentinel
-        __syncthreads();
-        RunList A;
-        A.q = sg.act;
-        A.kr = sg.actkr;
-        run_stepped(P, sg, B, S, W1, L, A, st, t_lim);
-        __syncthreads();
-        for (int x = lane; x < L.ln; x += 64) {
-            Fg[x] = L.F[x];
-            Qg[x] = L.Q[x];
-        }
-        st.ln = L.ln;
-        st.lq = L.tot;
     } else if (LIST) {
         const int cap = P.list_cap;
         int32_t* Fg = P.lst_f + (int64_t)g * P.list_stride;
@@ -1777,7 +1852,7 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
             A.q = sg.act;
             A.kr = sg.actkr;
             RingStep<D_LDS> R(D);
-            run_stepped(P, sg, B, S, W1, R, A, st, t_lim);
+            run_stepped<false>(P, sg, B, S, W1, R, A, st, t_lim);
         } else {
             RingProf<D_LDS> R(D, uni(st.t));
             run_known(P, sg, B, S, W1, R, st, t_lim);
@@ -1804,9 +1879,16 @@ void k_sim_list(SimArgs P) {
     sim_segment<false, false, true>(P);
 }
 
-// The per-step path with the finish-ordered list.
+// The per-step path with the finish-ordered list: with room for the bound,
+// with less (segments may stop inside a step), and the continuation.
 __global__ __launch_bounds__(64) void k_sim_steplist(SimArgs P) {
     sim_segment<false, true, true>(P);
+}
+__global__ __launch_bounds__(64) void k_sim_steplist_stop(SimArgs P) {
+    sim_segment<false, true, true, false, true>(P);
+}
+__global__ __launch_bounds__(64) void k_sim_steplist_resume(SimArgs P) {
+    sim_segment<false, true, true, true>(P);
 }
 
 // The same for the continuation of segments whose list outgrew the first
@@ -1964,7 +2046,9 @@ hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool li
                       size_t lds_bytes, hipStream_t s) {
     if (G <= 0) return hipSuccess;
     if (stepped && list) {
-        hipLaunchKernelGGL(k_sim_steplist, dim3(G), dim3(64), lds_bytes, s, P);
+        if (P.list_resume) hipLaunchKernelGGL(k_sim_steplist_resume, dim3(G), dim3(64), lds_bytes, s, P);
+        else if (P.list_cap < P.list_stride) hipLaunchKernelGGL(k_sim_steplist_stop, dim3(G), dim3(64), lds_bytes, s, P);
+        else hipLaunchKernelGGL(k_sim_steplist, dim3(G), dim3(64), lds_bytes, s, P);
     } else if (!stepped && list) {
         if (P.list_resume) hipLaunchKernelGGL(k_sim_list_resume, dim3(G), dim3(64), lds_bytes, s, P);
         else hipLaunchKernelGGL(k_sim_list, dim3(G), dim3(64), lds_bytes, s, P);
@@ -1994,6 +2078,8 @@ hipError_t prepare_sim(bool d_lds, size_t lds_ring, bool list, size_t lds_list) 
     }
     if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_list, lds_list);
     if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_steplist, lds_list);
+    if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_steplist_resume, lds_list);
+    if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_steplist_stop, lds_list);
     if (e == hipSuccess && list) e = sim_attr((const void*)k_sim_list_resume, lds_list);
     return e;
 }
@@ -2002,6 +2088,13 @@ hipError_t sim_known_occupancy(bool list, bool d_lds, size_t lds_bytes, int* blo
     const void* f = list ? (const void*)k_sim_list
                          : (d_lds ? (const void*)k_sim<true, false>
                                   : (const void*)k_sim<false, false>);
+    hipError_t e = sim_attr(f, lds_bytes);
+    if (e != hipSuccess) return e;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, f, 64, lds_bytes);
+}
+
+hipError_t sim_step_occupancy(size_t lds_bytes, int* blocks) {
+    const void* f = (const void*)k_sim_steplist_stop;
     hipError_t e = sim_attr(f, lds_bytes);
     if (e != hipSuccess) return e;
     return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, f, 64, lds_bytes);

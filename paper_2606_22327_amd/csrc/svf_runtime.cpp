@@ -68,7 +68,9 @@ struct svf_batch {
     size_t lds_list = 0;      // LDS of the event kernel with the list
     size_t lds_list_full = 0; //   and with room for the bound (continuation)
     bool list_stepped = false; // per-step path: profile as the finish-ordered list
+    int32_t step_cap = 0;      // its entries in LDS (first launch)
     size_t lds_step = 0;       // LDS of the per-step kernel with the list
+    size_t lds_step_full = 0;  //   and with room for the bound (continuation)
     int32_t kbits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t bw_total = 0;
     bool d_lds = true;
@@ -394,9 +396,18 @@ int do_sim(svf_batch* h, int64_t delta) {
             HIPCHK(svfk::launch_sim(S, G, false, false, true, h->lds_list_full, h->stream));
         }
     }
-    if (h->n_stepped > 0)
+    if (h->n_stepped > 0) {
+        S.list_cap = h->step_cap;
+        S.list_resume = 0;
         HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, h->list_stepped,
                                 h->list_stepped ? h->lds_step : h->lds_bytes, h->stream));
+        if (h->list_stepped && h->step_cap < h->list_stride) {
+            // segments whose list outgrew the LDS capacity, up to the same step
+            S.list_cap = h->list_stride;
+            S.list_resume = 1;
+            HIPCHK(svfk::launch_sim(S, G, false, true, true, h->lds_step_full, h->stream));
+        }
+    }
     record_end(h, 1, e0);
     h->sim_launches += 1;
     h->dirty = true;
@@ -579,15 +590,34 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
         }
     }
     // The per-step path keeps its planned profile as the finish-ordered list
-    // (room for the bound, no continuation) when that fits in 64 KB of LDS.
+    // when the list with room for the bound fits in 64 KB of LDS.  As on the
+    // event path, the first launch gives it the largest capacity that keeps
+    // the kernel at the occupancy its registers allow, and a continuation
+    // launch has room for the bound.
     if (h->any_stepped) {
         const char* ps = getenv("SVFSIM_STEP_PROFILE");
         bool use = full_bytes <= 64 * 1024;
         if (ps && !strcmp(ps, "ring")) use = false;
         if (ps && !strcmp(ps, "list")) use = full_bytes <= 160 * 1024;
         if (use) {
+            auto occ = [&](size_t bytes) {
+                int w = 0;
+                return svfk::sim_step_occupancy(bytes, &w) == hipSuccess ? w : -1;
+            };
+            const int w_top = occ(bm_bytes + (size_t)svfk::list_slots(64) * 8);
+            int64_t lo = std::min<int64_t>(bound, 64), hi = bound;
+            while (w_top > 0 && lo < hi) {
+                const int64_t mid = lo + (hi - lo + 1) / 2;
+                if (occ(bm_bytes + (size_t)svfk::list_slots((int)mid) * 8) >= w_top) lo = mid;
+                else hi = mid - 1;
+            }
+            int64_t cap = w_top > 0 ? lo : bound;
+            const char* pc = getenv("SVFSIM_STEP_LDS_CAP");  // testing: a smaller LDS list
+            if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
             h->list_stepped = true;
-            h->lds_step = full_bytes;
+            h->step_cap = (int32_t)cap;
+            h->lds_step = bm_bytes + (size_t)svfk::list_slots((int)cap) * 8;
+            h->lds_step_full = full_bytes;
         }
     }
     if (h->list_known || h->list_stepped) h->list_stride = (int32_t)bound;
@@ -662,7 +692,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess) {
         hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes, h->list_known || h->list_stepped,
-                                         std::max(h->lds_list_full, h->lds_step));
+                                         std::max(h->lds_list_full, h->lds_step_full));
         if (a != hipSuccess) e = a;
     }
     if (e == hipSuccess && h->fused_sort) {

@@ -345,13 +345,19 @@ def test_event_path_both_profiles(profile):
         os.environ.pop("SVFSIM_LIST_LDS_CAP", None)
 
 
-@pytest.mark.parametrize("profile", ["ring", "list"])
+@pytest.mark.parametrize("profile", ["ring", "list", "list-lds7", "list-lds64"])
 def test_stepped_path_both_profiles(profile):
     """The per-step path (1-bit SVF, predicted lengths, next-step admission)
     keeps the planned profile either in the ring or in the finish-ordered
     list (early completions and evictions remove entries from its middle).
-    Each forced on the same batches, against the oracle, also step by step."""
-    os.environ["SVFSIM_STEP_PROFILE"] = profile
+    Each forced on the same batches, against the oracle, also step by step.
+    The list-ldsN cases give the list in LDS room for only N entries, so
+    segments stop inside the admission phase of a step and the continuation
+    launch resumes them there."""
+    os.environ["SVFSIM_STEP_PROFILE"] = profile.split("-")[0]
+    cap = int(profile.split("lds")[1]) if "lds" in profile else None
+    if cap:
+        os.environ["SVFSIM_STEP_LDS_CAP"] = str(cap)
     try:
         b3 = W.config(3, instances=24, n=600)
         say(f"step profile {profile}: config 3 reduced")
@@ -373,8 +379,11 @@ def test_stepped_path_both_profiles(profile):
             gr = gpu_run(r)
             for pol in r.policies:
                 compare(r, gr[pol], pol, label=f"{profile}-random{seed}")
+        if cap:
+            assert max_concurrent(b3, g3["svf1bit"]) > cap, "no list outgrew the LDS room"
     finally:
         del os.environ["SVFSIM_STEP_PROFILE"]
+        os.environ.pop("SVFSIM_STEP_LDS_CAP", None)
 
 
 def test_degenerate_cases():
