@@ -790,8 +790,8 @@ __device__ __forceinline__ void fold_range(const Ring<LDS>& R, int lo, int hi, i
 // ordered by planned finish (ListProf).  Both offer begin (at each visited
 // step, before admissions), fit (the forward-looking check of a candidate
 // started at t, and its admission when it fits; *t_free as in fit_and_admit
-// otherwise), stopped (the segment has to leave the launch at the current
-// step) and end (the peak of the steps up to t).
+// otherwise, or -1: the segment has to leave the launch at the current step)
+// and end (the peak of the steps up to t).
 
 template <bool LDS>
 struct RingProf {
@@ -800,7 +800,6 @@ struct RingProf {
     int peak_lane;  // per-lane largest memory total of the folded steps
     __device__ __forceinline__ RingProf(const Ring<LDS>& d, int t) : D(d), folded(t), peak_lane(0) {}
     __device__ __forceinline__ void begin(int) {}
-    __device__ __forceinline__ bool stopped() const { return false; }
     __device__ __forceinline__ bool fit(int t, int s_h, int oh, int M, int maxF, int* t_free) {
         // slots up to t + oh must be labelled for the current window
         if (t + oh - D.H > folded) {
@@ -834,8 +833,9 @@ struct RingProf {
 // visited step; D at their finish step goes into the peak.  The host bounds
 // the requests that can run at once; the list in LDS may hold fewer (more
 // waves then fit on a compute unit).  A candidate that fits into a full list
-// stops the segment at that step (stopped(), with the candidate as the head
-// and t_f = t); a later launch with room for the bound continues it.
+// gets *t_free = -1 (a real failure always gives a step after t): the segment
+// stops at that step with the candidate as the head, and a later launch with
+// room for the bound continues it.
 //
 // Every lane of a group takes part in every step, so that no lane is masked
 // off (the scalar unit, which would juggle the masks, is the busiest unit of
@@ -853,9 +853,6 @@ struct ListProf {
     int ln;         // entries
     uint32_t tot;   // Q of the last entry (0 if none)
     int peak_lane;
-    bool may_stop;  // a full list stops the segment (else: the bound was wrong)
-    bool full;      // stopped on a full list
-    __device__ __forceinline__ bool stopped() const { return full; }
     __device__ __forceinline__ void begin(int t) {
         const int lane = lane_id();
         while (ln > 0) {
@@ -930,8 +927,7 @@ struct ListProf {
             return false;
         }
         if (ln >= cap) {
-            full = may_stop;
-            *t_free = may_stop ? t : INT32_MAX;
+            *t_free = -1;
             return false;
         }
         // the entries c .. ln-1 move up by one and gain s_h - t, group by
@@ -1139,8 +1135,9 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
             }
         }
 
-        // the candidate is the head, checked again at t when the segment resumes
-        if (prof.stopped()) break;
+        // a full list: the candidate is the head, checked again at t when the
+        // segment resumes
+        if (t_f < 0) break;
 
         // 5. advance to the next step where anything can happen: with a
         //    blocked head, its release or the next arrival ranked above it
@@ -1811,8 +1808,6 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
         L.ln = uni(st.ln);
         L.tot = (uint32_t)uni((int)st.lq);
         L.peak_lane = 0;
-        L.may_stop = cap < P.list_stride;
-        L.full = false;
         if (P.list_resume) t_lim = st.resume_lim;
         st.resume_lim = 0;
         if (L.ln > cap) {
@@ -1824,6 +1819,8 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
                 L.Q[x] = Qg[x];
             }
             if (L.ln == 0 && lane == 0) L.F[0] = INT32_MAX;  // the empty list's sentinel
+            // a stop on a full list left t_f = -1: the head is checked again at t
+            if (st.t_f < 0) st.t_f = st.t;
             __syncthreads();
             run_known(P, sg, B, S, W1, L, st, t_lim);
             __syncthreads();
@@ -1833,7 +1830,7 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
             }
             st.ln = L.ln;
             st.lq = L.tot;
-            if (L.full) st.resume_lim = t_lim;
+            if (st.t_f < 0) st.resume_lim = t_lim;  // stopped on a full list
         }
     } else {
         const int RS = P.H + 64;  // ring stride: H slots and the spare slot, padded
