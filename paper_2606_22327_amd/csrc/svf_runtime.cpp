@@ -539,14 +539,17 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     if (env && !strcmp(env, "lds") && ring_bytes + bm_bytes <= 160 * 1024) h->d_lds = true;
     h->lds_bytes = std::max<size_t>(8, bm_bytes + (h->d_lds ? ring_bytes : 0));
     // The event path keeps its profile as the finish-ordered list (8 bytes
-    // per running request) in LDS when the ring does not fit there, or when
-    // the ring's LDS is what limits the waves resident on a compute unit, the
-    // list lets more of them reside and there are more segments than the
-    // ring lets reside at once.  Elsewhere the ring's shorter per-event work
-    // wins.  The list in LDS gets
-    // the largest capacity that still lets as many waves reside as the list
-    // kernel's registers allow; segments that outgrow it stop, and a second
-    // launch with room for the bound on concurrent requests continues them.
+    // per running request) when the ring does not fit in LDS, or when few
+    // requests run at once: the list's checks and insertions touch the
+    // running requests that finish before the candidate, the ring's the
+    // candidate's whole planned length.  Measured: the list is faster at
+    // about 140-280 concurrent requests (4096 x 1000 and 16384 x 5000
+    // workloads), 4x slower at about 930 (64 x 200,000); the estimate is
+    // M / (mean s + mean o / 2) and the crossover is taken at 512.  The list
+    // in LDS gets the largest capacity that still lets as many waves reside
+    // as the list kernel's registers allow; segments that outgrow it stop,
+    // and a second launch with room for the bound on concurrent requests
+    // continues them.
     const int64_t bound = (h->n_known > 0 || h->any_stepped)
                               ? std::max<int64_t>(1, running_bound(v.s, off, d->M)) : 1;
     const size_t full_bytes = bm_bytes + (size_t)svfk::list_slots((int)std::min<int64_t>(bound, 1 << 24)) * 8;
@@ -569,16 +572,13 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
             cap = lo;
             const char* pc = getenv("SVFSIM_LIST_LDS_CAP");  // testing: a smaller LDS list
             if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
-            const int w_ring = occ(false, h->d_lds, h->lds_bytes);
-            const int w_regs = occ(false, h->d_lds, bm_bytes);
-            const int w_list = occ(true, false, bm_bytes + (size_t)svfk::list_slots((int)cap) * 8);
-            int cus = 0;
-            if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->device) != hipSuccess)
-                cus = 0;
-            const int64_t segs = (int64_t)h->n_known;
-            if (w_top > 0 && w_ring >= 0 && w_regs >= 0 && w_list > 0)
-                use = !h->d_lds ||
-                      (w_ring < w_regs && w_list > w_ring && segs > (int64_t)w_ring * cus);
+            double sum_s = 0.0, sum_o = 0.0;
+            for (int64_t x = 0; x < N; ++x) {
+                sum_s += v.s[x];
+                sum_o += v.o[x];
+            }
+            const double running = N > 0 ? (double)d->M / ((sum_s + 0.5 * sum_o) / (double)N) : 0.0;
+            if (w_top > 0) use = !h->d_lds || running <= 512.0;
         }
         if (pe && !strcmp(pe, "ring")) use = false;
         if (pe && !strcmp(pe, "list")) use = full_bytes <= 160 * 1024;
