@@ -42,6 +42,24 @@ def kernel_source_digest():
     return hashlib.sha256(data).hexdigest()[:16]
 
 
+def issue_from_profile(workload):
+    """Instruction-issue fractions of the simulation kernel (rocprofv3 SQ
+    counters against one SALU and one VALU instruction per CU per cycle), if
+    recorded for this workload and the current kernels; None otherwise
+    (profiles/issue_<workload>.json)."""
+    p = os.path.join(ROOT, "profiles", f"issue_{workload}.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        d = json.load(open(p))
+    except Exception:
+        return None
+    if d.get("kernel_source_sha256_16") != kernel_source_digest():
+        return None
+    return {"salu_frac": round(d["salu_issue_frac"], 3), "valu_frac": round(d["valu_issue_frac"], 3),
+            "basis": d["peak_basis"], "source": f"profiles/issue_{workload}.json"}
+
+
 def traffic_from_profile(workload):
     """HBM bytes per simulation launch measured with rocprofv3 counters
     (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy kernel's reading),
@@ -173,6 +191,7 @@ def main():
         if args.predictor_sigma is not None:
             workload += f"-sigma{args.predictor_sigma:g}"
     traffic = traffic_from_profile(workload)
+    issue = issue_from_profile(workload)
 
     out = {
         "metric": "simulated request-steps/sec at 1 GPU",
@@ -197,7 +216,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "k_sim", "kernel_avg_ms": sim_avg_s * 1000.0,
-                     "algorithmic_bytes_per_launch": b_alg},
+                     "algorithmic_bytes_per_launch": b_alg, "issue": issue},
         "kernel_ms": {"init": tm["init_ms"] / args.steps, "sim": tm["sim_ms"] / args.steps,
                       "final": tm["final_ms"] / args.steps},
     }
