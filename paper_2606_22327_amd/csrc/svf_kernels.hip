@@ -468,6 +468,14 @@ __device__ __forceinline__ int wmin(int v) {
     return __builtin_amdgcn_readlane(v, 63);
 }
 
+// One record at a uniform index, loaded through the scalar cache: the records
+// are written by the sort before the simulation and only read while it runs.
+__device__ __forceinline__ int4 record(const int4* rec, int r) {
+    typedef __attribute__((address_space(4))) const int cint;
+    const cint* p = (const cint*)(rec + r);
+    return make_int4(p[0], p[1], p[2], p[3]);
+}
+
 __device__ __forceinline__ int4 readlane4(const int4& v, int src) {
     int4 r;
     r.x = __builtin_amdgcn_readlane(v.x, src);
@@ -1006,17 +1014,8 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     };
     load_arrivals(cursor);
 
-    // Rank window: lane l holds the record of rank rwb + l (rwb a multiple of
-    // 64, so one window covers one bitmap word).
-    int rwb = INT32_MIN / 2;
-    int4 rw = make_int4(0, 0, 0, 0);
-    auto rec_of = [&](int r) -> int4 {
-        if ((unsigned)(r - rwb) >= 64u) {
-            rwb = uni(r & ~63);
-            rw = sg.rec[min(rwb + lane, n - 1)];  // lanes past the end: a copy
-        }
-        return readlane4(rw, r - rwb);
-    };
+    // the record of one rank: a scalar load (read-only while the simulation runs)
+    auto rec_of = [&](int r) -> int4 { return record(sg.rec, r); };
     int4 hq = make_int4(0, 0, 0, 0);  // record of the blocked head
     if (head >= 0) hq = rec_of(head);
     // Admissions are staged in registers, lane j holding the j-th of up to 64
@@ -1426,16 +1425,8 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         }
     };
     load_arrivals(cursor);
-    // rank window: lane l holds the record of rank rwb + l
-    int rwb = INT32_MIN / 2;
-    int4 rw = make_int4(0, 0, 0, 0);
-    auto rec_of = [&](int r) -> int4 {
-        if (r < rwb || r >= rwb + 64) {
-            rwb = uni(r & ~63);
-            rw = sg.rec[min(rwb + lane, n - 1)];
-        }
-        return readlane4(rw, r - rwb);
-    };
+    // the record of one rank: a scalar load (read-only while the simulation runs)
+    auto rec_of = [&](int r) -> int4 { return record(sg.rec, r); };
     // Steps that provably change nothing are not scanned or checked:
     //  - next_ev: no running request completes or reaches its planned length
     //    before this step (the list is scanned only from then on);
@@ -1678,7 +1669,7 @@ __device__ void stepped_resume_tail(const SimArgs& P, const Seg& sg, uint64_t* B
     for (;;) {
         const int r = bitmap_first(B, S, W1);
         if (r < 0) break;
-        const int4 q = sg.rec[r];
+        const int4 q = record(sg.rec, r);
         if (D.next(t) + extra1 + q.y + 1 > M) break;
         int tf = 0;
         if (!D.fit(t, q.y, q.z, M, extra1, maxF, &tf, chk)) break;
