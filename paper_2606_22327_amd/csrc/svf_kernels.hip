@@ -36,7 +36,12 @@
 // candidate h at step t (no future step above M; Appendix E.2) is then one
 // pass over its own window: max_{j<o^_h} D[t+1+j] + (s_h + j + 1) <= M.
 // Admitting h adds its growth to the same window; a step that becomes past is
-// folded into the peak statistic and cleared.
+// folded into the peak statistic and cleared.  The other form of the profile
+// is the list of running requests ordered by planned finish, with prefix sums
+// of s - k: between admissions the memory only drops at finishes, so the
+// check visits just the finishes inside the candidate's window and its last
+// step (ListProf, StepList).  The host picks the form per batch: the list
+// where few requests run at once, the ring where many do.
 //
 // Known lengths (the scheduler plans with the true length) make D change only
 // at admissions, so a blocked head stays blocked until a computable step t_f
