@@ -2021,6 +2021,8 @@ hipError_t prepare_sort_rec(int max_n) {
     if (max_n <= 128 * 8) return sort_rec_attr<128, 8>();
     if (max_n <= 128 * 16) return sort_rec_attr<128, 16>();
     if (max_n <= 256 * 16) return sort_rec_attr<256, 16>();
+    if (max_n <= 256 * 20) return sort_rec_attr<256, 20>();
+    if (max_n <= 256 * 24) return sort_rec_attr<256, 24>();
     if (max_n <= 256 * 32) return sort_rec_attr<256, 32>();
     return hipErrorInvalidValue;
 }
@@ -2031,6 +2033,8 @@ hipError_t launch_sort_rec(const SortArgs& A, int G, int max_n, hipStream_t s) {
     if (max_n <= 128 * 8) return sort_rec_go<128, 8>(A, G, s);
     if (max_n <= 128 * 16) return sort_rec_go<128, 16>(A, G, s);
     if (max_n <= 256 * 16) return sort_rec_go<256, 16>(A, G, s);
+    if (max_n <= 256 * 20) return sort_rec_go<256, 20>(A, G, s);
+    if (max_n <= 256 * 24) return sort_rec_go<256, 24>(A, G, s);
     if (max_n <= 256 * 32) return sort_rec_go<256, 32>(A, G, s);
     return hipErrorInvalidValue;
 }

@@ -237,8 +237,9 @@ def test_ragged_sizes_with_merge_passes():
 
 def test_fused_sort_shapes_boundary_and_wide_keys():
     """Instances sorted by the one-workgroup radix sort in each of its
-    workgroup shapes (largest instance 200, 1000, 2000, 4000 and exactly 8192
-    requests), the first size past it (8193, sorted in chunks and merged),
+    workgroup shapes (largest instance 200, 1000, 2000, 4000, 5000, exactly
+    5120, 6144 and 8192 requests, and one past the first two), the first size
+    past the largest (8193, sorted in chunks and merged),
     and SVF keys just below 2^32 (eight radix passes) next to tiny ones."""
     rng = np.random.default_rng(2606)
 
@@ -247,7 +248,7 @@ def test_fused_sort_shapes_boundary_and_wide_keys():
         return {"arrival": a, "prompt": rng.integers(1, s_hi + 1, n),
                 "output": rng.integers(1, o_hi + 1, n)}
 
-    for top in (200, 1000, 2000, 4000, 8192, 8193):
+    for top in (200, 1000, 2000, 4000, 5000, 5120, 5121, 6144, 6145, 8192, 8193):
         sizes = [top, 0, 1, max(1, top // 3), 7]
         parts = [part(n, 300, 400, 0.3) for n in sizes]
         b = W.assemble(f"shape{top}", parts, 4096, ("svf", "sjf", "fcfs"))
