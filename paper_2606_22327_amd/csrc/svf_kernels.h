@@ -100,6 +100,7 @@ struct SimArgs {
     int32_t list_stride;      // entries per segment in HBM (bound on concurrent requests)
     int32_t list_cap;         // entries per segment in LDS in this launch (<= list_stride)
     int32_t list_resume;      // 1: only continue the segments that stopped with a full list
+    int32_t resident;         // workgroups of this launch resident at once (0: no issue priorities)
 };
 
 struct FinArgs {
@@ -139,6 +140,8 @@ hipError_t launch_sim(const SimArgs& P, int G, bool d_lds, bool stepped, bool li
 hipError_t sim_known_occupancy(bool list, bool d_lds, size_t lds_bytes, int* blocks);
 // resident waves per compute unit of the per-step kernel with the list
 hipError_t sim_step_occupancy(size_t lds_bytes, int* blocks);
+// resident waves per compute unit of the first simulation kernel of a path
+hipError_t sim_occupancy(bool stepped, bool list, bool d_lds, size_t lds_bytes, int* blocks);
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s);
 
 }  // namespace svfk

@@ -473,6 +473,44 @@ __device__ __forceinline__ int wmin(int v) {
     return __builtin_amdgcn_readlane(v, 63);
 }
 
+// Issue priority of a wave by the progress of its slot.  A launch of G
+// single-wave workgroups holds `resident` of them on the GPU at once, and the
+// hardware starts them in order of blockIdx, so workgroup g runs in round
+// g / resident of R = ceil(G / resident), in a slot that a workgroup of the
+// round before has freed.  At equal priority the arbiter favours older waves:
+// the oldest waves of a round finish first, their slots start the next round
+// early, and the last round drains as a long tail of ever fewer waves.  Here
+// the slot's progress (round + done / n) / R selects one of the four levels,
+// higher while less is done, so that the slots advance together and the last
+// round ends at about the same time everywhere.  Issue order changes only
+// timing: every output is the same at any priority.
+struct IssuePrio {
+    int64_t base, den;  // progress numerator at done = 0, and its denominator (R n)
+    int next;           // done count at which the level drops next
+
+    __device__ __forceinline__ void init(int resident, int n, int done) {
+        next = INT32_MAX;
+        if (resident <= 0 || n <= 0) return;
+        const int rnd = (int)blockIdx.x / resident;
+        const int R = ((int)gridDim.x + resident - 1) / resident;
+        base = (int64_t)rnd * n;
+        den = (int64_t)R * n;
+        set(done);
+    }
+    __device__ __forceinline__ void set(int done) {
+        const int q = (int)(((base + done) * 4) / den);
+        if (q <= 0) __builtin_amdgcn_s_setprio(3);
+        else if (q == 1) __builtin_amdgcn_s_setprio(2);
+        else if (q == 2) __builtin_amdgcn_s_setprio(1);
+        else __builtin_amdgcn_s_setprio(0);
+        // smallest done with (base + done) * 4 >= (q + 1) den
+        next = q >= 3 ? INT32_MAX : (int)(((q + 1) * den + 3) / 4 - base);
+    }
+    __device__ __forceinline__ void update(int done) {
+        if (done >= next) set(done);
+    }
+};
+
 // One record at a uniform index, loaded through the scalar cache: the records
 // are written by the sort before the simulation and only read while it runs.
 __device__ __forceinline__ int4 record(const int4* rec, int r) {
@@ -1028,6 +1066,8 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     // admission numbers, so that no store is in flight behind each admission;
     // the finish (start + o) is derived when the outputs are finalised.
     int stg_idx = 0, stg_t = 0, nstg = 0;
+    IssuePrio prio;
+    prio.init(P.resident, n, seq0);
     auto flush = [&]() {
         if (lane < nstg) {
             sg.start[stg_idx] = stg_t;
@@ -1035,6 +1075,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         }
         seq0 += nstg;
         nstg = 0;
+        prio.update(seq0);
     };
 
     // Bitmap word of the current candidate, mirrored in scalar registers for
@@ -1446,6 +1487,8 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     int next_ev = t;  // scan at the first step of a launch
     int blk = -1, blk_tf = 0;
     bool relaxed = true;
+    IssuePrio prio;
+    prio.init(P.resident, n, nfin);
 
     for (;;) {
         if (nfin == n) { status = STATUS_DONE; break; }
@@ -1528,6 +1571,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             N_O += (int)wave_sum_i64(dN);
             if (dfin > 0) relaxed = true;
             nfin += dfin;
+            prio.update(nfin);
             next_ev = wmin(nxt);
             RunList::order();  // the compacted list is read again below
         }
@@ -2085,6 +2129,16 @@ hipError_t sim_known_occupancy(bool list, bool d_lds, size_t lds_bytes, int* blo
     const void* f = list ? (const void*)k_sim_list
                          : (d_lds ? (const void*)k_sim<true, false>
                                   : (const void*)k_sim<false, false>);
+    hipError_t e = sim_attr(f, lds_bytes);
+    if (e != hipSuccess) return e;
+    return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, f, 64, lds_bytes);
+}
+
+hipError_t sim_occupancy(bool stepped, bool list, bool d_lds, size_t lds_bytes, int* blocks) {
+    const void* f;
+    if (list) f = stepped ? (const void*)k_sim_steplist : (const void*)k_sim_list;
+    else if (stepped) f = d_lds ? (const void*)k_sim<true, true> : (const void*)k_sim<false, true>;
+    else f = d_lds ? (const void*)k_sim<true, false> : (const void*)k_sim<false, false>;
     hipError_t e = sim_attr(f, lds_bytes);
     if (e != hipSuccess) return e;
     return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, f, 64, lds_bytes);

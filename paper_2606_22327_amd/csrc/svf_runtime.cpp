@@ -71,6 +71,8 @@ struct svf_batch {
     int32_t step_cap = 0;      // its entries in LDS (first launch)
     size_t lds_step = 0;       // LDS of the per-step kernel with the list
     size_t lds_step_full = 0;  //   and with room for the bound (continuation)
+    int32_t res_known = 0;     // workgroups resident at once: first event launch
+    int32_t res_stepped = 0;   //   and first per-step launch (0: no issue priorities)
     int32_t kbits[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     int64_t bw_total = 0;
     bool d_lds = true;
@@ -384,6 +386,7 @@ int do_sim(svf_batch* h, int64_t delta) {
     S.list_stride = h->list_stride;
     S.list_cap = h->list_cap;
     S.list_resume = 0;
+    S.resident = h->res_known;
     hipEvent_t e0 = nullptr;
     record(h, 1, &e0);
     if (h->n_known > 0) {
@@ -393,18 +396,21 @@ int do_sim(svf_batch* h, int64_t delta) {
             // segments whose list outgrew the LDS capacity, up to the same step
             S.list_cap = h->list_stride;
             S.list_resume = 1;
+            S.resident = 0;
             HIPCHK(svfk::launch_sim(S, G, false, false, true, h->lds_list_full, h->stream));
         }
     }
     if (h->n_stepped > 0) {
         S.list_cap = h->step_cap;
         S.list_resume = 0;
+        S.resident = h->res_stepped;
         HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, h->list_stepped,
                                 h->list_stepped ? h->lds_step : h->lds_bytes, h->stream));
         if (h->list_stepped && h->step_cap < h->list_stride) {
             // segments whose list outgrew the LDS capacity, up to the same step
             S.list_cap = h->list_stride;
             S.list_resume = 1;
+            S.resident = 0;
             HIPCHK(svfk::launch_sim(S, G, false, true, true, h->lds_step_full, h->stream));
         }
     }
@@ -622,6 +628,27 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     }
     if (h->list_known || h->list_stepped) h->list_stride = (int32_t)bound;
     h->ring_used = (h->n_known > 0 && !h->list_known) || (h->any_stepped && !h->list_stepped);
+    // Resident workgroups of the first simulation launch of each path: the
+    // kernels order the issue priorities of their waves by it (timing only).
+    {
+        int ncu = 0;
+        const char* pp = getenv("SVFSIM_ISSUE_PRIO");  // "0": all waves at one priority
+        const bool on = !(pp && !strcmp(pp, "0"));
+        if (on && hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess &&
+            ncu > 0) {
+            int w = 0;
+            if (h->n_known > 0 &&
+                svfk::sim_occupancy(false, h->list_known, h->d_lds,
+                                    h->list_known ? h->lds_list : h->lds_bytes, &w) == hipSuccess)
+                h->res_known = w * ncu;
+            w = 0;
+            if (h->any_stepped &&
+                svfk::sim_occupancy(true, h->list_stepped, h->d_lds,
+                                    h->list_stepped ? h->lds_step : h->lds_bytes, &w) == hipSuccess)
+                h->res_stepped = w * ncu;
+        }
+        (void)hipGetLastError();
+    }
     if (h->lds_bytes > 160 * 1024) {
         delete h;
         return fail(SVF_EINVAL, "an instance's rank bitmap needs %zu bytes of LDS (> 160 KB)", h->lds_bytes);

@@ -495,6 +495,27 @@ def _sample(n_inst, k, seed):
     return ids
 
 
+def test_issue_priorities_do_not_change_results(monkeypatch):
+    """More segments than the GPU holds at once (several rounds of resident
+    workgroups), on the event and the per-step path: outputs with the waves'
+    issue priorities set by their progress equal those with one priority for
+    all, and the oracle's."""
+    b = W.random_small(77, instances=12000, n_max=30, s_max=12, o_max=20, M=60,
+                       gap_mean=0.3, bits=True)
+    b.policies = ("svf", "svf1bit", "sjf+cur")
+    b.max_steps = W.default_max_steps(b)
+    say("issue priorities: 12000 x <= 30 requests, 3 policies, priorities on")
+    on = gpu_run(b)
+    monkeypatch.setenv("SVFSIM_ISSUE_PRIO", "0")
+    say("issue priorities off")
+    off = gpu_run(b)
+    for pol in b.policies:
+        for f in FIELDS:
+            assert np.array_equal(on[pol][f], off[pol][f]), (pol, f)
+        assert np.array_equal(on[pol]["stats"], off[pol]["stats"]), pol
+        compare(b, on[pol], pol, label="prio")
+
+
 def test_full_config2_sampled():
     b = W.config(2)
     say("full config 2: 4096 x 1000 x 3 policies")
