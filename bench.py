@@ -32,14 +32,16 @@ def log(msg):
 
 
 def kernel_source_digest():
-    """Digest of what the kernels are built from: their source and the GPU
-    compiler flags."""
+    """Digest of what the kernels and their launches are built from: the
+    kernel source and header, the runtime that chooses launch shapes, LDS
+    capacities and issue priorities, and the GPU compiler flags."""
     import hashlib
     from paper_2606_22327_amd import build as B
 
-    src = os.path.join(ROOT, "paper_2606_22327_amd", "csrc", "svf_kernels.hip")
-    data = open(src, "rb").read() + " ".join(B.GPU_FLAGS).encode()
-    return hashlib.sha256(data).hexdigest()[:16]
+    csrc = os.path.join(ROOT, "paper_2606_22327_amd", "csrc")
+    data = b"".join(open(os.path.join(csrc, f), "rb").read()
+                    for f in ("svf_kernels.hip", "svf_kernels.h", "svf_runtime.cpp"))
+    return hashlib.sha256(data + " ".join(B.GPU_FLAGS).encode()).hexdigest()[:16]
 
 
 def issue_from_profile(workload):

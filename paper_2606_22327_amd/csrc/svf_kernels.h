@@ -101,6 +101,7 @@ struct SimArgs {
     int32_t list_cap;         // entries per segment in LDS in this launch (<= list_stride)
     int32_t list_resume;      // 1: only continue the segments that stopped with a full list
     int32_t resident;         // workgroups of this launch resident at once (0: no issue priorities)
+    unsigned long long* prog; // [1] progress counter of this launch, cleared before it
 };
 
 struct FinArgs {

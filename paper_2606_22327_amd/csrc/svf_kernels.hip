@@ -473,41 +473,64 @@ __device__ __forceinline__ int wmin(int v) {
     return __builtin_amdgcn_readlane(v, 63);
 }
 
-// Issue priority of a wave by the progress of its slot.  A launch of G
-// single-wave workgroups holds `resident` of them on the GPU at once, and the
-// hardware starts them in order of blockIdx, so workgroup g runs in round
-// g / resident of R = ceil(G / resident), in a slot that a workgroup of the
-// round before has freed.  At equal priority the arbiter favours older waves:
-// the oldest waves of a round finish first, their slots start the next round
-// early, and the last round drains as a long tail of ever fewer waves.  Here
-// the slot's progress (round + done / n) / R selects one of the four levels,
-// higher while less is done, so that the slots advance together and the last
-// round ends at about the same time everywhere.  Issue order changes only
-// timing: every output is the same at any priority.
+// Issue priority of a wave by its remaining work.  A launch runs one
+// single-wave workgroup per segment, more of them than the GPU holds at once;
+// the hardware starts them in order of blockIdx as slots free up.  At equal
+// priority the arbiter favours older waves, so the last waves to start are
+// the last to finish and the launch drains as a long tail of ever fewer
+// waves, which issue far less per cycle than a full CU.  Instead the waves
+// keep one counter per launch: the number of running waves and the sum of
+// their remaining requests (admissions still to make, or requests still to
+// finish), updated every 32 requests and when a wave starts and ends.  A
+// wave with more remaining than the mean gets a higher level (four levels,
+// 1/64 of its segment apart): remaining work evens out, and the waves that
+// are running when the last ones start end at about the same time.  The
+// counter value used is the one returned by the wave's previous update, so
+// no wave waits for it.  Issue order changes only timing: every output is
+// the same at any priority.
 struct IssuePrio {
-    int64_t base, den;  // progress numerator at done = 0, and its denominator (R n)
-    int next;           // done count at which the level drops next
+    static constexpr int SH = 40;  // counter: running waves << SH | sum of remaining
+    unsigned long long* ctr;
+    unsigned long long pend;       // the counter as returned by the last update (lane 0)
+    int n, th, next, last;
 
-    __device__ __forceinline__ void init(int resident, int n, int done) {
+    __device__ __forceinline__ void add(unsigned long long v) {
+        if (lane_id() == 0) pend = atomicAdd(ctr, v);
+    }
+    __device__ __forceinline__ void init(const SimArgs& P, int n_, int done) {
         next = INT32_MAX;
-        if (resident <= 0 || n <= 0) return;
-        const int rnd = (int)blockIdx.x / resident;
-        const int R = ((int)gridDim.x + resident - 1) / resident;
-        base = (int64_t)rnd * n;
-        den = (int64_t)R * n;
-        set(done);
+        ctr = nullptr;
+        if (P.resident <= 0 || n_ <= 0 || P.prog == nullptr || done >= n_) return;
+        ctr = P.prog;
+        n = n_;
+        th = max(n / 64, 1);
+        last = done;
+        pend = 0ull;
+        add((1ull << SH) + (unsigned long long)(n - done));
+        next = done + 32;
+        __builtin_amdgcn_s_setprio(2);
     }
     __device__ __forceinline__ void set(int done) {
-        const int q = (int)(((base + done) * 4) / den);
-        if (q <= 0) __builtin_amdgcn_s_setprio(3);
-        else if (q == 1) __builtin_amdgcn_s_setprio(2);
-        else if (q == 2) __builtin_amdgcn_s_setprio(1);
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)pend);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(pend >> 32));
+        const uint64_t c = ((uint64_t)hi << 32) | lo;
+        const int64_t cnt = (int64_t)(c >> SH), sum = (int64_t)(c & ((1ull << SH) - 1ull));
+        // (my remaining - mean remaining) * cnt, against the level step * cnt
+        const int64_t d = (int64_t)(n - done) * cnt - sum, s = (int64_t)th * cnt;
+        if (d > s) __builtin_amdgcn_s_setprio(3);
+        else if (d > 0) __builtin_amdgcn_s_setprio(2);
+        else if (d > -s) __builtin_amdgcn_s_setprio(1);
         else __builtin_amdgcn_s_setprio(0);
-        // smallest done with (base + done) * 4 >= (q + 1) den
-        next = q >= 3 ? INT32_MAX : (int)(((q + 1) * den + 3) / 4 - base);
+        add(0ull - (unsigned long long)(done - last));
+        last = done;
+        next = done + 32;
     }
     __device__ __forceinline__ void update(int done) {
         if (done >= next) set(done);
+    }
+    // the wave leaves the count (every exit of the simulation loop)
+    __device__ __forceinline__ void leave() {
+        if (ctr != nullptr) add(0ull - ((1ull << SH) + (unsigned long long)(n - last)));
     }
 };
 
@@ -1067,7 +1090,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     // the finish (start + o) is derived when the outputs are finalised.
     int stg_idx = 0, stg_t = 0, nstg = 0;
     IssuePrio prio;
-    prio.init(P.resident, n, seq0);
+    prio.init(P, n, seq0);
     auto flush = [&]() {
         if (lane < nstg) {
             sg.start[stg_idx] = stg_t;
@@ -1205,6 +1228,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         t = uni(nt);
     }
     flush();
+    prio.leave();
     // the peak over the steps up to t
     const int pk = prof.end(t);
     st.t = t; st.cursor = cursor; st.seq = seq0; st.nfin = seq0; st.max_fin = max_fin;
@@ -1488,7 +1512,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
     int blk = -1, blk_tf = 0;
     bool relaxed = true;
     IssuePrio prio;
-    prio.init(P.resident, n, nfin);
+    prio.init(P, n, nfin);
 
     for (;;) {
         if (nfin == n) { status = STATUS_DONE; break; }
@@ -1694,6 +1718,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         D.end_step(t);
         ++t;
     }
+    prio.leave();
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nfin; st.nA = nA; st.N_O = N_O;
     st.C_O = C_O; st.peak = peak; st.req_steps = req_steps; st.status = status;
     st.max_fin = maxF;

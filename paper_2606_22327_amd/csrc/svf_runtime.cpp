@@ -107,6 +107,7 @@ struct svf_batch {
     StatsOut* d_stats = nullptr;
     int32_t* d_lst_f = nullptr;
     uint32_t* d_lst_q = nullptr;
+    unsigned long long* d_prog = nullptr;  // [2] progress counters of the simulation launches
     const uint64_t* sorted_keys = nullptr;  // which key buffer holds the final order
 };
 
@@ -130,7 +131,7 @@ void free_all(svf_batch* h) {
                     h->d_chunk_seg, h->d_chunk_lo, h->d_keys0, h->d_keys1, h->d_rec,
                     h->d_rank, h->d_stepped, h->d_bw_off, h->d_bitmap, h->d_ring,
                     h->d_start, h->d_fin, h->d_pre, h->d_seq, h->d_act, h->d_actkr, h->d_evl,
-                    h->d_st, h->d_fin_out, h->d_stats, h->d_lst_f, h->d_lst_q};
+                    h->d_st, h->d_fin_out, h->d_stats, h->d_lst_f, h->d_lst_q, h->d_prog};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     for (auto& t : h->timed) {
@@ -387,6 +388,8 @@ int do_sim(svf_batch* h, int64_t delta) {
     S.list_cap = h->list_cap;
     S.list_resume = 0;
     S.resident = h->res_known;
+    S.prog = h->d_prog;
+    HIPCHK(svfk::launch_fill_u64(reinterpret_cast<uint64_t*>(h->d_prog), 2, 0ull, h->stream));
     hipEvent_t e0 = nullptr;
     record(h, 1, &e0);
     if (h->n_known > 0) {
@@ -404,6 +407,7 @@ int do_sim(svf_batch* h, int64_t delta) {
         S.list_cap = h->step_cap;
         S.list_resume = 0;
         S.resident = h->res_stepped;
+        S.prog = h->d_prog + 1;
         HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, h->list_stepped,
                                 h->list_stepped ? h->lds_step : h->lds_bytes, h->stream));
         if (h->list_stepped && h->step_cap < h->list_stride) {
@@ -628,14 +632,15 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     }
     if (h->list_known || h->list_stepped) h->list_stride = (int32_t)bound;
     h->ring_used = (h->n_known > 0 && !h->list_known) || (h->any_stepped && !h->list_stepped);
-    // Resident workgroups of the first simulation launch of each path: the
-    // kernels order the issue priorities of their waves by it (timing only).
+    // Resident workgroups of the first simulation launch of each path; the
+    // waves set their issue priorities only when it is known (timing only).
+    // With at most one segment per CU there is nothing to arbitrate.
     {
         int ncu = 0;
         const char* pp = getenv("SVFSIM_ISSUE_PRIO");  // "0": all waves at one priority
         const bool on = !(pp && !strcmp(pp, "0"));
         if (on && hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess &&
-            ncu > 0) {
+            ncu > 0 && (int64_t)P * I > ncu) {
             int w = 0;
             if (h->n_known > 0 &&
                 svfk::sim_occupancy(false, h->list_known, h->d_lds,
@@ -692,6 +697,7 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
         ALLOC(d_evl, PN);
     }
     ALLOC(d_st, G);
+    ALLOC(d_prog, 2);
     ALLOC(d_fin_out, PN);
     ALLOC(d_stats, G);
 #undef ALLOC
