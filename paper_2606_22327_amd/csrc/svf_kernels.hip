@@ -1258,10 +1258,17 @@ struct RingStep {
         return fit_and_admit(D, t, s_h, oh, M, extra1, maxF, t_free, chk);
     }
     __device__ __forceinline__ void remove(int t, int s, int k, int L) { remove_future(D, t, s, k, L); }
-    __device__ __forceinline__ void end_step(int t) {
-        // the slot of step t+1 becomes the one of step t+1+H (nothing planned yet)
+    // the next step is tn > t: the slots of steps t+1 .. tn become those of
+    // steps t+1+H .. tn+H (nothing is planned that far; the last H of them
+    // when more than H steps pass)
+    __device__ __forceinline__ void end_step(int t, int tn) {
         Ring<LDS>::order();
-        if (lane_id() == 0) D.st(t + 1, t + 1 + D.H);
+        const int J = tn - t;
+        if (J == 1) {
+            if (lane_id() == 0) D.st(t + 1, t + 1 + D.H);
+        } else {
+            for (int x = max(J - D.H, 0) + lane_id(); x < J; x += 64) D.st(t + 1 + x, t + 1 + x + D.H);
+        }
         Ring<LDS>::order();
     }
 };
@@ -1447,7 +1454,7 @@ struct StepList {
             lds_order();
         }
     }
-    __device__ __forceinline__ void end_step(int) {}
+    __device__ __forceinline__ void end_step(int, int) {}
 };
 
 
@@ -1518,9 +1525,11 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         if (nfin == n) { status = STATUS_DONE; break; }
         if (t > P.max_steps) { status = STATUS_EXHAUSTED; break; }
         if (t >= t_lim) break;
-        // 1. arrivals: a prefix of the window (arrivals are sorted)
+        // 1. arrivals up to t: a prefix of the window (arrivals are sorted;
+        //    those of earlier steps were ranked below the blocked head, which
+        //    stayed blocked, so nothing could happen at their steps)
         for (;;) {
-            const bool arr = (wb + lane >= cursor) && (a_reg == t);
+            const bool arr = (wb + lane >= cursor) && (a_reg <= t);
             const uint64_t m = ballot(arr);
             if (m == 0ull) break;
             if (arr) bitmap_set_atomic(B, S, rk_reg);
@@ -1711,12 +1720,41 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             lds_order();
             relaxed = true;  // one of them may rank above the blocked head
         }
-        // 5. advance
-        req_steps += nA;
+        // 5. advance to the next step at which anything can happen.  Until
+        //    then no request arrives, completes, reaches its planned length or
+        //    is evicted, no request ranked above the blocked head arrives (with
+        //    nothing waiting: no request arrives), and the blocked head stays
+        //    blocked, so every running request grows by one token per step:
+        //    the true memory at step tau+1 is mem + nA (tau - t), below M
+        //    until tau_ov.  Evicted requests compete again at t+1, and a
+        //    segment whose requests have all finished ends at t+1.
         const int64_t mem = planned_next() + C_O + (int64_t)N_O * (t + 1);
-        peak = max(peak, mem);
-        D.end_step(t);
-        ++t;
+        int tn = t + 1;
+        if (nev == 0 && nfin < n) {
+            int tj = min(next_ev, min(t_lim, P.max_steps + 1));
+            if (cursor < n) {
+                int na;
+                if (blk >= 0) {  // the next arrival ranked above the head (past the window: its end)
+                    const uint64_t up = ballot((wb + lane >= cursor) && rk_reg < blk);
+                    na = up != 0ull ? __builtin_amdgcn_readlane(a_reg, __builtin_ctzll(up))
+                                    : (wb + 64 < n ? uni(sg.a[wb + 64]) : INT32_MAX);
+                } else {
+                    na = cursor < wb + 64 ? __builtin_amdgcn_readlane(a_reg, cursor - wb)
+                                          : uni(sg.a[cursor]);
+                }
+                tj = min(tj, na);
+            }
+            if (blk >= 0) tj = min(tj, blk_tf);
+            if (nA > 0 && tj > t + 1) {
+                const int64_t room = (int64_t)M - mem;  // >= 0 after the admissions
+                tj = room < 0 ? t + 1 : min(tj, t + 1 + (int)((uint32_t)room / (uint32_t)nA));
+            }
+            tn = max(tj, t + 1);
+        }
+        req_steps += (int64_t)nA * (tn - t);
+        peak = max(peak, mem + (int64_t)nA * (tn - 1 - t));
+        D.end_step(t, tn);
+        t = uni(tn);
     }
     prio.leave();
     st.t = t; st.cursor = cursor; st.seq = seq; st.nfin = nfin; st.nA = nA; st.N_O = N_O;
@@ -1768,7 +1806,7 @@ __device__ void stepped_resume_tail(const SimArgs& P, const Seg& sg, uint64_t* B
     }
     st.req_steps += nA;
     st.peak = max(st.peak, D.next(t) + C_O + (int64_t)N_O * (t + 1));
-    D.end_step(t);
+    D.end_step(t, t + 1);
     st.t = t + 1;
     st.seq = seq;
     st.nA = nA;
