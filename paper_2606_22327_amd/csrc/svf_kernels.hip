@@ -1031,11 +1031,9 @@ struct ListProf {
                 shift(b, tp, F[jj], Q[jj]);
             }
         }
-        if (c == 0) {  // no entry before the candidate
-            if (lane == 0) {
-                F[0] = te;
-                Q[0] = qn;
-            }
+        if (c == 0) {  // no entry before the candidate (every lane stores the same values)
+            F[0] = te;
+            Q[0] = qn;
         }
         lds_order();
         ++ln;
@@ -1170,10 +1168,9 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                 }
                 if (++nstg == 64) flush();
                 cbits &= ~(1ull << (r & 63));
-                if (lane == 0) {
-                    B[cw] = cbits;
-                    if (cbits == 0ull) S[cw >> 6] &= ~(1ull << (cw & 63));
-                }
+                // every lane stores the same word (no lane mask to set up)
+                B[cw] = cbits;
+                if (cbits == 0ull) S[cw >> 6] &= ~(1ull << (cw & 63));
                 lds_order();
                 max_fin = max(max_fin, t + q.w);
                 // Once every arrival ranked above the old head is running, the
@@ -1182,15 +1179,14 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                 // since t_f was computed, which can only delay the release.
                 // (Candidates come in rank order, so the first n_below of them
                 // are exactly those arrivals.)
-                if (n_below > 0) {
-                    if (--n_below == 0) {
-                        if (old_head == INT32_MAX) { head = -1; break; }
-                        if (t < t_f) break;
-                        r = old_head;
-                        q = hq0;
-                        if (cw != (r >> 6)) load_word(r >> 6);
-                        continue;
-                    }
+                // (n_below <= 0 stays below zero)
+                if (--n_below == 0) {
+                    if (old_head == INT32_MAX) { head = -1; break; }
+                    if (t < t_f) break;
+                    r = old_head;
+                    q = hq0;
+                    if (cw != (r >> 6)) load_word(r >> 6);
+                    continue;
                 }
                 if (cbits != 0ull) {
                     r = cw * 64 + __builtin_ctzll(cbits);
