@@ -1996,9 +1996,17 @@ void k_sim_list_resume(SimArgs P) {
 
 // ------------------------------------------------------------ finalize
 
-__global__ __launch_bounds__(64) void k_finalize(FinArgs F) {
+// One workgroup of FIN_NT threads per segment, FIN_U requests per thread in
+// flight: the outputs are a streaming pass over start, o and a (plus the
+// per-step path's finish and preemption counts, which the event path never
+// writes: its finish is start + o and it never evicts).
+constexpr int FIN_NT = 256, FIN_U = 4;
+
+__global__ __launch_bounds__(FIN_NT) void k_finalize(FinArgs F) {
+    __shared__ long long red[3][FIN_NT / 64];
+    __shared__ int redm[FIN_NT / 64];
     const int g = blockIdx.x;
-    const int lane = lane_id();
+    const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
     const int pol = g / F.I, inst = g - pol * F.I;
     const int64_t off = F.offsets[inst];
     const int n = (int)(F.offsets[inst + 1] - off);
@@ -2008,24 +2016,56 @@ __global__ __launch_bounds__(64) void k_finalize(FinArgs F) {
     const int t_end = st.t;
     long long lat = 0, rs = 0, pre = 0;
     int mk = 0;
-    for (int j = lane; j < n; j += 64) {
-        const int k = F.start[base + j];
-        // known lengths: the finish is start + o (not stored by the simulation)
-        int f = stepped ? F.fin[base + j] : (k >= 0 ? k + F.o[off + j] : -1);
-        if (f > t_end - 1) f = -1;
-        F.fin_out[base + j] = f;
-        if (f >= 0) {
-            lat += (long long)f - F.a[off + j];
-            mk = max(mk, f);
+    for (int j0 = 0; j0 < n; j0 += FIN_NT * FIN_U) {
+        int k[FIN_U], o[FIN_U], a[FIN_U], f[FIN_U], p[FIN_U];
+#pragma unroll
+        for (int u = 0; u < FIN_U; ++u) {
+            const int j = j0 + u * FIN_NT + tid;
+            k[u] = -1; o[u] = 0; a[u] = 0; f[u] = -1; p[u] = 0;
+            if (j < n) {
+                k[u] = F.start[base + j];
+                o[u] = F.o[off + j];
+                a[u] = F.a[off + j];
+                if (stepped) {
+                    f[u] = F.fin[base + j];
+                    p[u] = F.preempt[base + j];
+                }
+            }
         }
-        if (!stepped && k >= 0) rs += (long long)min(k + F.o[off + j], t_end) - k;
-        pre += F.preempt[base + j];
+#pragma unroll
+        for (int u = 0; u < FIN_U; ++u) {
+            const int j = j0 + u * FIN_NT + tid;
+            if (j >= n) continue;
+            // known lengths: the finish is start + o (not stored by the simulation)
+            int fj = stepped ? f[u] : (k[u] >= 0 ? k[u] + o[u] : -1);
+            if (fj > t_end - 1) fj = -1;
+            F.fin_out[base + j] = fj;
+            if (fj >= 0) {
+                lat += (long long)fj - a[u];
+                mk = max(mk, fj);
+            }
+            if (!stepped && k[u] >= 0) rs += (long long)min(k[u] + o[u], t_end) - k[u];
+            pre += p[u];
+        }
     }
     lat = wave_sum_i64(lat);
     rs = wave_sum_i64(rs);
     pre = wave_sum_i64(pre);
     mk = wave_max_i32(mk);
     if (lane == 0) {
+        red[0][w] = lat;
+        red[1][w] = rs;
+        red[2][w] = pre;
+        redm[w] = mk;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int x = 1; x < FIN_NT / 64; ++x) {
+            lat += red[0][x];
+            rs += red[1][x];
+            pre += red[2][x];
+            mk = max(mk, redm[x]);
+        }
         StatsOut so;
         so.makespan = mk;
         so.status = st.status;
@@ -2212,7 +2252,7 @@ hipError_t sim_step_occupancy(size_t lds_bytes, int* blocks) {
 
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s) {
     if (G <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_finalize, dim3(G), dim3(64), 0, s, F);
+    hipLaunchKernelGGL(k_finalize, dim3(G), dim3(FIN_NT), 0, s, F);
     return hipGetLastError();
 }
 
