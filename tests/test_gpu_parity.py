@@ -495,6 +495,30 @@ def _sample(n_inst, k, seed):
     return ids
 
 
+@pytest.mark.parametrize("kw", [dict(bits=True), dict(plan_noise=True)], ids=["onebit", "noisy"])
+def test_stepped_jumps_across_launch_limits(kw):
+    """The per-step path jumps from one step at which something can happen to
+    the next (arrivals ranked above the blocked head, completions, planned
+    lengths running out, the first overflow of M, the head's release step);
+    a launch's step limit cuts a jump short.  Runs in irregular step chunks
+    equal one run to completion, and the oracle, in every output and
+    statistic (request-steps and peak memory included)."""
+    b = W.random_small(404, instances=60, n_max=80, s_max=16, o_max=40, M=90,
+                       gap_mean=0.7, **kw)
+    b.policies = ("svf1bit", "svf", "sjf+cur") if kw.get("bits") else ("svf", "sjf", "fcfs+cur")
+    b.max_steps = W.default_max_steps(b)
+    say(f"stepped jumps {kw}: one run")
+    whole = gpu_run(b)
+    say(f"stepped jumps {kw}: chunks")
+    chunks = [1, 2, 3, 5, 8, 13, 21, 34, 55, 89] * 4 + [10 ** 9]
+    parts = gpu_run(b, chunks=chunks)
+    for pol in b.policies:
+        for f in FIELDS:
+            assert np.array_equal(whole[pol][f], parts[pol][f]), (pol, f)
+        assert np.array_equal(whole[pol]["stats"], parts[pol]["stats"]), pol
+        compare(b, whole[pol], pol, label=f"jumps{kw}")
+
+
 def test_issue_priorities_do_not_change_results(monkeypatch):
     """More segments than the GPU holds at once (several rounds of resident
     workgroups), on the event and the per-step path: outputs with the waves'
