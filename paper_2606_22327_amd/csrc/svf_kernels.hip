@@ -16,10 +16,11 @@
 //   k_sim<D_LDS, STEPPED>, k_sim_list, k_sim_list_resume, k_sim_steplist,
 //   k_sim_steplist_stop, k_sim_steplist_resume
 //                     the simulation: one wave64 per segment (profile as a ring,
-//                     per-step or event-driven; or as a finish-ordered list)
+//                     per-step or event-driven; or as a finish-ordered list);
+//                     the waves order their issue priorities by remaining work
 //   k_finalize        per-request outputs as of the reached step (finish derived
 //                     as start + o where lengths are known) + per-segment
-//                     statistics
+//                     statistics, one 256-thread workgroup per segment
 //
 // Waiting set.  A segment's requests are sorted once by priority; the waiting
 // set is then a bitmap over priority ranks (bit r set iff the request of rank
@@ -49,10 +50,12 @@
 // or until a request of higher priority arrives.  Such segments jump from
 // event to event; the skipped steps are exactly the ones where the per-step
 // scheduler admits nothing.  Segments whose planned lengths differ from the
-// truth (1-bit SVF, noisy predictions) are advanced one step at a time: they
-// track true completions, requests running past their planned length (planned
-// to finish at the next step, kept as two running sums), and evictions when the
-// true memory of the next step would exceed M.
+// truth (1-bit SVF, noisy predictions) are advanced step by step: they track
+// true completions, requests running past their planned length (planned to
+// finish at the next step, kept as two running sums), and evictions when the
+// true memory of the next step would exceed M; they too jump over the steps
+// at which none of these can happen (memory then grows by one token per
+// running request per step).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
