@@ -52,6 +52,7 @@ struct SortArgs {
     const int32_t* plan;      // [N] or null
     const int8_t* bit;        // [N] or null
     const int32_t* policies;  // [P] (device)
+    const uint8_t* stepped;   // [G] 1: per-step path (its finishes and preemptions are cleared too)
     const int32_t* chunk_seg; // [nchunks] segment of each chunk
     const int32_t* chunk_lo;  // [nchunks] first rank position of each chunk
     const uint64_t* keys_in;  // [P*N]

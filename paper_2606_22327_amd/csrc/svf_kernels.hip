@@ -285,6 +285,7 @@ __global__ __launch_bounds__(NT) void k_sort_rec(SortArgs A) {
     const int64_t off = A.offsets[inst];
     const int n = (int)(A.offsets[inst + 1] - off);
     const int policy = A.policies[pol] & 0xFF;
+    const bool stepped = A.stepped[g] != 0;
     const int tid = threadIdx.x;
     const int lane = tid & 63, w = tid >> 6;
     const int64_t base = (int64_t)pol * A.N + off;
@@ -398,9 +399,11 @@ __global__ __launch_bounds__(NT) void k_sort_rec(SortArgs A) {
             }
             if (r < n) {
                 A.start[base + r] = -1;
-                A.fin[base + r] = -1;
-                A.preempt[base + r] = 0;
                 A.admit_seq[base + r] = -1;
+                if (stepped) {  // the event path never writes these (cleared at creation)
+                    A.fin[base + r] = -1;
+                    A.preempt[base + r] = 0;
+                }
             }
         }
     }

@@ -325,6 +325,7 @@ int do_reset(svf_batch* h) {
         A.I = h->I; A.P = h->P; A.N = h->N; A.O0 = h->O0; A.O1 = h->O1; A.CH = h->CH;
         for (int p = 0; p < 8; ++p) A.kbits[p] = h->kbits[p];
         A.start = h->d_start; A.fin = h->d_fin; A.preempt = h->d_pre; A.admit_seq = h->d_seq;
+        A.stepped = h->d_stepped;
         if (h->fused_sort) {
             // keys, sort, records, ranks and cleared outputs in one kernel
             HIPCHK(svfk::launch_sort_rec(A, G, h->max_n, h->stream));
@@ -722,6 +723,11 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     CPY(h->d_stepped, stepped.data(), G, hipMemcpyHostToDevice);
     CPY(h->d_bw_off, bw_off.data(), 8 * (I + 1), hipMemcpyHostToDevice);
 #undef CPY
+    // Finishes and preemption counts are written only by the per-step path;
+    // event-path segments keep these initial values (the reset's sort clears
+    // them for per-step segments only).
+    if (e == hipSuccess) e = svfk::launch_fill_i32(h->d_fin, PN, -1, h->stream);
+    if (e == hipSuccess) e = svfk::launch_fill_i32(h->d_pre, PN, 0, h->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e == hipSuccess) {
         hipError_t a = svfk::prepare_sim(h->d_lds, h->lds_bytes, h->list_known || h->list_stepped,
