@@ -1466,8 +1466,11 @@ struct StepList {
 struct RunList {
     int4* q;
     int2* kr;
-    // entries written by one lane are read by others next
-    __device__ __forceinline__ static void order() { __syncthreads(); }
+    // Entries written by one lane are read by others next.  The list is read
+    // and written by the lanes of one wave only, which see
+    // each other's memory operations in program order without waiting; the
+    // fence keeps the compiler from reordering them.
+    __device__ __forceinline__ static void order() { lds_order(); }
 };
 
 // STOP: the profile may fill up (a list with less room than the host's
@@ -1714,7 +1717,7 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         }
         // evicted requests compete again from the next step
         if (nev > 0) {
-            __syncthreads();  // their ranks were stored by lane 0
+            lds_order();  // their ranks were stored by lane 0 of this wave
             for (int x = lane; x < nev; x += 64) {
                 const int r = sg.evl[x];
                 if ((unsigned)r < (unsigned)n) bitmap_set_atomic(B, S, r);
@@ -1889,7 +1892,7 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
             A.q = sg.act;
             A.kr = sg.actkr;
             if (RESUME && mid >= 0) {
-                __syncthreads();  // the evicted ranks were stored by lane 0
+                lds_order();  // the evicted ranks were stored by lane 0 of this wave
                 stepped_resume_tail(P, sg, B, S, W1, L, A, st, mid);
             }
             run_stepped<STOP>(P, sg, B, S, W1, L, A, st, t_lim);
