@@ -150,6 +150,11 @@ typedef struct svf_timing {
 } svf_timing;
 
 /*
+ * Build a batch of instances.  An instance is the problem of Section 3.1:
+ * requests (a_i, s_i, o_i) and a budget M, with the start steps as the
+ * decisions of the integer program (the x_{i,t} of eq:c1) and the policy's
+ * order of Section 2.2 (Eq. 1, Eq. 2, SJF, FCFS).
+ *
  * Validate ``desc`` on the host and build a handle: allocates the device
  * buffers and copies the inputs (host-to-device, or device-to-device when
  * inputs_on_device).  ``hip_stream`` is a hipStream_t (NULL: the null stream)
@@ -161,6 +166,10 @@ typedef struct svf_timing {
 int svf_create(const svf_batch_desc *desc, void *hip_stream, svf_batch **out);
 
 /*
+ * Process 1 of Alg. 1 / Alg. 2 (every request's priority from its prompt and
+ * believed length: the volume of Eq. 1, its 1-bit form Eq. 2, or the SJF and
+ * FCFS keys), for all requests up front.
+ *
  * Asynchronous.  Restart every instance and policy slot at step 0: computes
  * the priority keys (Eq. 1 / Eq. 2), sorts each instance's requests by
  * (key, arrival, index) and clears the per-instance state.
@@ -168,6 +177,12 @@ int svf_create(const svf_batch_desc *desc, void *hip_stream, svf_batch **out);
 int svf_reset(svf_batch *h);
 
 /*
+ * The discrete decode steps of Section 3.1 (one token per running request
+ * per step, constraint eq:c2 on the memory of every step), each one pass of
+ * the scheduling loop of Alg. 1 / Alg. 2, Process 2: arrivals, completions,
+ * eviction on overflow, strict head-of-line admission under the
+ * forward-looking check, advance.
+ *
  * Asynchronous.  Advance every unfinished instance by ``nsteps`` simulated
  * steps (nsteps >= 0), or until it finishes or passes max_steps.  Calls
  * svf_reset first if the handle was never reset.  State stays on the GPU
@@ -176,12 +191,20 @@ int svf_reset(svf_batch *h);
 int svf_step(svf_batch *h, int64_t nsteps);
 
 /*
+ * The same loop (Alg. 1 / Alg. 2, Process 2, over the steps of Section 3.1)
+ * until every request has finished: the schedule whose total latency is the
+ * objective eq:obj.
+ *
  * Asynchronous.  Run every instance from its current step to completion (or
  * max_steps).  Calls svf_reset first if the handle was never reset.
  */
 int svf_run(svf_batch *h);
 
 /*
+ * The decisions and their outcome per request (Section 3.1): the start step
+ * k_i chosen by the scheduler and the finish k_i + o_i whose difference to
+ * a_i is the request's latency in the objective eq:obj.
+ *
  * Copy the per-request results of policy slot ``policy_slot`` (an index into
  * desc.policies) into caller buffers of N int32 each, for the state reached so
  * far (synchronises the stream when outputs_on_device == 0):
@@ -197,8 +220,15 @@ int svf_read(svf_batch *h, int32_t policy_slot, int32_t *start, int32_t *finish,
              int32_t *preempt, int32_t *admit_seq, int32_t outputs_on_device);
 
 /*
+ * Per-instance aggregates of the schedule: the total latency of eq:obj
+ * (sum of finish - a_i, exact in 64 bits), the largest memory of any step
+ * (at most M by eq:c2), request-steps (running requests summed over steps,
+ * one token each per step), the makespan (duration behind the throughput of
+ * Section 4.1) and the eviction count.
+ *
  * Copy per-instance statistics of policy slot ``policy_slot`` into ``out``
- * (host array [num_instances]); synchronises the stream.
+ * (host array [num_instances]); synchronises the stream.  Errors: SVF_EINVAL
+ * (slot out of range, NULL ``out``), SVF_ESTATE (never reset), SVF_EHIP.
  */
 int svf_stats(svf_batch *h, int32_t policy_slot, svf_instance_stats *out);
 

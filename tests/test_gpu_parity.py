@@ -23,6 +23,8 @@ from oracle import validate
 from paper_2606_22327_amd import svfsim as S
 from paper_2606_22327_amd import workloads as W
 
+import hand_cases
+
 pytestmark = pytest.mark.gpu
 
 FIELDS = ("start", "finish", "preempt", "admit_seq")
@@ -385,6 +387,34 @@ def test_stepped_path_both_profiles(profile):
     finally:
         del os.environ["SVFSIM_STEP_PROFILE"]
         os.environ.pop("SVFSIM_STEP_LDS_CAP", None)
+
+
+@pytest.mark.parametrize("profile", ["ring", "list"])
+def test_eviction_hand_worked_cases(profile):
+    """The hand-worked eviction instances (tests/golden/eviction_cases.txt)
+    through the C ABI, compared with the values derived by hand (not with the
+    oracle): each case replicated over 300 instances of one launch, run to the
+    end or stopped by svf_step before the case's stop step, with the per-step
+    path's planned profile forced to the ring or to the finish-ordered list."""
+    os.environ["SVFSIM_STEP_PROFILE"] = profile
+    try:
+        for case in hand_cases.load():
+            one = case["batch"]
+            reps = 300
+            b = W.assemble(case["name"], [one.instance(0)] * reps, one.M, one.policies,
+                           O0=one.O0, O1=one.O1)
+            say(f"hand case {case['name']} ({case['policy']}), profile {profile}")
+            chunks = None if case["t_stop"] is None else [case["t_stop"]]
+            g = gpu_run(b, chunks=chunks)[case["policy"]]
+            n = int(one.offsets[1])
+            for f, want in case["expected"].items():
+                got = g[f].reshape(reps, n)
+                assert (got == want[None, :]).all(), (case["name"], f, got[0].tolist())
+            for f in SFIELDS:
+                got = g["stats"][f].astype(np.int64)
+                assert (got == case["stats"][f]).all(), (case["name"], f, int(got[0]))
+    finally:
+        del os.environ["SVFSIM_STEP_PROFILE"]
 
 
 def test_degenerate_cases():

@@ -16,6 +16,8 @@ import oracle
 from oracle import bounds, literal, opt, validate
 from paper_2606_22327_amd import workloads as W
 
+import hand_cases
+
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
@@ -548,3 +550,40 @@ def test_poisson_bounds_shape():
     _, _, e600 = bounds.poisson_conditional_proxies(mu, 600)
     _, _, e1000 = bounds.poisson_conditional_proxies(mu, 1000)
     assert e1000 < e600 < e200 < ev
+
+
+# --------------------------------------- eviction path (a3), hand-worked
+
+def _hand_case_ids():
+    return [c["name"] for c in hand_cases.load()]
+
+
+@pytest.mark.parametrize("name", _hand_case_ids())
+def test_eviction_hand_worked_cases(name):
+    """The eviction step against instances derived by hand from the rule
+    (tests/golden/eviction_cases.txt): victim = largest believed remaining
+    volume sum_{x=e+1..max(o^, e+1)} (s + x), ties to the latest arrival,
+    progress lost (the restart runs the whole true length), eligible again only
+    from the next step, evictions repeated until the next step fits; plus the
+    current-capacity rule and the 1-bit proxies.  Expected start, finish,
+    eviction count, admission order and every statistic are the hand values."""
+    case = next(c for c in hand_cases.load() if c["name"] == name)
+    b = case["batch"]
+    kw = {} if case["t_stop"] is None else {"t_stop": case["t_stop"]}
+    r = oracle.run(b, case["policy"], threads=1, **kw)
+    for f, want in case["expected"].items():
+        assert r[f].tolist() == want.tolist(), (name, f)
+    got = dict(zip(oracle.STAT_FIELDS, r["stats"][0].tolist()))
+    assert got == case["stats"], name
+
+
+def test_eviction_hand_cases_literal_agrees():
+    for case in hand_cases.load():
+        b = case["batch"]
+        d = b.instance(0)
+        L = literal.simulate(d["arrival"], d["prompt"], d["output"], b.M, case["policy"],
+                             plan=d["plan_len"], long_bit=d["long_bit"], O0=b.O0, O1=b.O1,
+                             max_steps=b.max_steps,
+                             t_stop=case["t_stop"] if case["t_stop"] is not None else 10 ** 18)
+        for f, want in case["expected"].items():
+            assert L[f] == want.tolist(), (case["name"], f)
