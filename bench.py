@@ -23,6 +23,12 @@ sys.path.insert(0, ROOT)
 import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+# Scalar issue: each compute unit issues at most one scalar (SALU) instruction
+# per cycle, so 256 CUs at the 2.4 GHz peak engine clock issue 614.4e9 per s.
+CUS, CLOCK_HZ = 256, 2.4e9
+SALU_PEAK_GIPS = CUS * CLOCK_HZ / 1e9
+# Byte model of a time-stepped simulator (every running request visited every
+# step): reported for comparison only, never as a share of any peak.
 BYTES_PER_REQUEST_STEP = 12    # read (s, k, L) of a running request per step
 BYTES_PER_REQUEST = 60         # inputs 12 + outputs 16 + packed key write/read 32
 
@@ -45,10 +51,10 @@ def kernel_source_digest():
 
 
 def issue_from_profile(workload):
-    """Instruction-issue fractions of the simulation kernel (rocprofv3 SQ
-    counters against one SALU and one VALU instruction per CU per cycle), if
-    recorded for this workload and the current kernels; None otherwise
-    (profiles/issue_<workload>.json)."""
+    """Instructions the simulation kernel issues per launch (rocprofv3 SQ
+    counters SQ_INSTS_SALU and SQ_INSTS_VALU, deterministic for a given kernel
+    and workload), if recorded for this workload and the current kernels; None
+    otherwise (profiles/issue_<workload>.json)."""
     p = os.path.join(ROOT, "profiles", f"issue_{workload}.json")
     if not os.path.exists(p):
         return None
@@ -58,8 +64,10 @@ def issue_from_profile(workload):
         return None
     if d.get("kernel_source_sha256_16") != kernel_source_digest():
         return None
-    return {"salu_frac": round(d["salu_issue_frac"], 3), "valu_frac": round(d["valu_issue_frac"], 3),
-            "basis": d["peak_basis"], "source": f"profiles/issue_{workload}.json"}
+    c = d["counters"]
+    return {"salu": float(c["SQ_INSTS_SALU"]), "valu": float(c["SQ_INSTS_VALU"]),
+            "kernel": d["kernel"], "profiled_ms": d["kernel_ms"],
+            "source": f"profiles/issue_{workload}.json"}
 
 
 def traffic_from_profile(workload):
@@ -88,7 +96,17 @@ def make_batch(cfg, instances, policies, sigma):
     return b
 
 
-def cpu_baseline(cfg, sample_instances, threads, policies=None, sigma=None):
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def oracle_rate(cfg, sample_instances, threads, policies=None, sigma=None):
     import oracle
 
     b = make_batch(cfg, sample_instances, policies, sigma)
@@ -98,9 +116,40 @@ def cpu_baseline(cfg, sample_instances, threads, policies=None, sigma=None):
         r = oracle.run(b, pol, threads=threads)
         rs += int(r["stats"][:, 3].sum())
     dt = time.perf_counter() - t0
-    return {"value": rs / dt, "unit": "request-steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {sample_instances} instances of the same workload "
-                      f"({b.num_requests} requests, {rs} request-steps) in {dt:.1f} s"}
+    return rs / dt, (f"first {sample_instances} instances of the same workload "
+                     f"({b.num_requests} requests, {rs} request-steps) in {dt:.1f} s")
+
+
+def cpu_baseline(cfg, sample_instances, sample_1t, threads, policies=None, sigma=None):
+    """The oracle (plain C, one thread per group of instances) on the host:
+    ``threads`` threads over the first ``sample_instances`` instances, and one
+    thread over the first ``sample_1t``."""
+    v, desc = oracle_rate(cfg, sample_instances, threads, policies, sigma)
+    v1, desc1 = oracle_rate(cfg, sample_1t, 1, policies, sigma)
+    return {"value": v, "unit": "request-steps/s", "cores": threads, "kind": "oracle",
+            "sample": desc, "cpu_model": cpu_model(), "host_logical_cpus": os.cpu_count(),
+            "cpus_allowed": len(os.sched_getaffinity(0)),
+            "single_thread": {"value": v1, "unit": "request-steps/s", "cores": 1,
+                              "sample": desc1}}
+
+
+def copy_bandwidth(nbytes=2 << 30, reps=5):
+    """A plain device-to-device copy of ``nbytes``, timed with events on the
+    current stream: achieved (read + written) bytes per second."""
+    import torch
+
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src, dst
+    return 2 * nbytes / (ms / 1000.0) / 1e9
 
 
 def main():
@@ -115,7 +164,10 @@ def main():
                          "(suffix +cur: admission on the next step's memory only)")
     ap.add_argument("--predictor-sigma", type=float, default=None,
                     help="plan with predicted lengths o * LogNormal(0, sigma), rounded")
-    ap.add_argument("--cpu-sample", type=int, default=1024)
+    ap.add_argument("--cpu-sample", type=int, default=1024,
+                    help="instances for the oracle on all allowed host threads (at most 16)")
+    ap.add_argument("--cpu-sample-1t", type=int, default=64,
+                    help="instances for the single-thread oracle figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="after the timed steps, copy MIB MiB device-to-device three times "
@@ -186,7 +238,6 @@ def main():
     units_req = batch.num_requests * n_slots
     b_alg = BYTES_PER_REQUEST_STEP * units_rs + BYTES_PER_REQUEST * units_req
     sim_avg_s = tm["sim_ms"] / max(1, tm["sim_launches"]) / 1000.0
-    achieved = b_alg / sim_avg_s / 1e9
     workload = f"cfg{args.config}"
     if policies or args.predictor_sigma is not None:
         workload += "-" + "-".join(batch.policies).replace("+", "")
@@ -194,6 +245,37 @@ def main():
             workload += f"-sigma{args.predictor_sigma:g}"
     traffic = traffic_from_profile(workload)
     issue = issue_from_profile(workload)
+    copy_gbs = copy_bandwidth()
+    log(f"device-to-device copy: {copy_gbs:.0f} GB/s (read + write)")
+
+    # The simulation is bound by scalar instruction issue (uniform control flow
+    # runs on the scalar unit): achieved = scalar instructions of one launch
+    # (SQ_INSTS_SALU, from the committed counter profile of these kernels) over
+    # the launch time measured here with HIP events.
+    if issue is not None:
+        salu_gips = issue["salu"] / sim_avg_s / 1e9
+        roof = {"bound": "alu", "achieved": salu_gips, "peak": SALU_PEAK_GIPS,
+                "unit": "G scalar instructions/s", "frac": salu_gips / SALU_PEAK_GIPS}
+        valu_frac = issue["valu"] / sim_avg_s / (CUS * CLOCK_HZ)
+        roof_src = issue["source"]
+    else:
+        roof = {"bound": "alu", "achieved": None, "peak": SALU_PEAK_GIPS,
+                "unit": "G scalar instructions/s", "frac": None}
+        valu_frac = None
+        roof_src = None
+    roof.update({
+        "traffic": traffic,
+        "kernel": "k_sim", "kernel_avg_ms": sim_avg_s * 1000.0,
+        "basis": "one SALU instruction per CU per cycle, 256 CUs at 2.4 GHz",
+        "instructions_source": roof_src,
+        "valu_frac": valu_frac,
+        "hbm": {"achieved_GBps": traffic / sim_avg_s / 1e9 if traffic else None,
+                "peak_GBps": HBM_PEAK_GBS,
+                "frac": traffic / sim_avg_s / 1e9 / HBM_PEAK_GBS if traffic else None,
+                "copy_GBps": copy_gbs},
+        "time_stepped_equivalent_GBps": b_alg / sim_avg_s / 1e9,
+        "time_stepped_bytes_per_launch": b_alg,
+    })
 
     out = {
         "metric": "simulated request-steps/sec at 1 GPU",
@@ -215,19 +297,17 @@ def main():
                    "requests": batch.num_requests, "policies": list(batch.policies),
                    "M": batch.M, "request_steps_per_step": req_steps,
                    "all_instances_done": status_ok},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "k_sim", "kernel_avg_ms": sim_avg_s * 1000.0,
-                     "algorithmic_bytes_per_launch": b_alg, "issue": issue},
+        "roofline": roof,
         "kernel_ms": {"init": tm["init_ms"] / args.steps, "sim": tm["sim_ms"] / args.steps,
                       "final": tm["final_ms"] / args.steps},
     }
     if not args.no_cpu_baseline:
-        threads = min(os.cpu_count() or 1, 16)
-        log(f"cpu baseline: oracle on {args.cpu_sample} instances, {threads} threads")
-        out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample, threads, policies,
-                                           args.predictor_sigma)
-        out["cpu_baseline"]["host"] = platform.processor() or platform.machine()
+        # one GPU's share of the host is 16 cores: at most 16 oracle threads
+        threads = min(len(os.sched_getaffinity(0)), 16)
+        log(f"cpu baseline: oracle on {args.cpu_sample} instances, {threads} threads; "
+            f"{args.cpu_sample_1t} instances on one thread")
+        out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample, args.cpu_sample_1t,
+                                           threads, policies, args.predictor_sigma)
     print(json.dumps(out))
 
 
