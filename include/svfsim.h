@@ -246,6 +246,53 @@ int svf_shape(const svf_batch *h, int64_t *num_requests, int32_t *num_instances,
  * Passing NULL is allowed and does nothing. */
 int svf_destroy(svf_batch *h);
 
+/*
+ * Limits of svf_run_noalloc: its device scratch per GPU (bytes), and the
+ * largest number of instances of one call.
+ */
+#define SVF_NOALLOC_SCRATCH_BYTES (128u << 20)
+#define SVF_NOALLOC_MAX_INSTANCES 65536
+
+/*
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * computation as svf_create + svf_run + svf_read / svf_stats of every policy
+ * slot, with every intermediate buffer (inputs staged on the device, priority
+ * records, rank bitmaps, memory profiles, running lists, per-segment state)
+ * carved from one static device array of SVF_NOALLOC_SCRATCH_BYTES per GPU,
+ * which the library holds until the process ends.  Calls no hipMalloc or
+ * hipFree and allocates no host memory.
+ *
+ *   desc       as for svf_create; the per-request arrays must be host memory
+ *              (inputs_on_device == 0), each instance must hold at most 8192
+ *              requests and num_instances <= SVF_NOALLOC_MAX_INSTANCES
+ *   hip_stream hipStream_t (NULL: the null stream) the work is enqueued on
+ *   start, finish, preempt, admit_seq
+ *              caller-owned device arrays of num_policies * N int32 each,
+ *              policy-slot major (slot p at [p * N, (p + 1) * N)), with the
+ *              meaning of svf_read's outputs after a run to completion
+ *   stats      caller-owned device array of num_policies * num_instances
+ *              svf_instance_stats, policy-slot major
+ *
+ * The inputs are copied into the scratch and the stream is synchronised
+ * before the call returns (the caller may then reuse its host arrays); the
+ * simulation and the outputs are asynchronous on ``hip_stream``.
+ *
+ * Every call on one GPU uses that GPU's single scratch array: calls that
+ * overlap on one GPU (on different streams, or from several threads) race
+ * and give undefined results; calls on one stream are ordered and safe.
+ * Each call clears and rebuilds everything it reads from the scratch.
+ *
+ * Errors: those of svf_create, and SVF_EINVAL when the batch needs more
+ * scratch than SVF_NOALLOC_SCRATCH_BYTES (the message gives both sizes),
+ * has an instance of more than 8192 requests or more than
+ * SVF_NOALLOC_MAX_INSTANCES instances, passes device inputs, or a NULL
+ * output for a non-empty batch.
+ */
+int svf_run_noalloc(const svf_batch_desc *desc, void *hip_stream, int32_t *start,
+                    int32_t *finish, int32_t *preempt, int32_t *admit_seq,
+                    svf_instance_stats *stats);
+
 /* Message of the calling thread's last non-zero return ("" if none). */
 const char *svf_last_error(void);
 

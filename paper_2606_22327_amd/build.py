@@ -36,11 +36,14 @@ def build(verbose: bool = False) -> str:
     rt_o = os.path.join(BUILD, "svf_runtime.o")
     _run(["hipcc", f"--offload-arch={ARCH}", *COMMON, *GPU_FLAGS, "-c",
           os.path.join(CSRC, "svf_kernels.hip"), "-o", kern_o])
+    na_o = os.path.join(BUILD, "svf_noalloc.o")
+    _run(["hipcc", f"--offload-arch={ARCH}", *COMMON, *GPU_FLAGS, "-c",
+          os.path.join(CSRC, "svf_noalloc.hip"), "-o", na_o])
     opt_o = os.path.join(BUILD, "svf_opt.o")
     _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "svf_runtime.cpp"), "-o", rt_o])
     _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "svf_opt.cpp"), "-o", opt_o])
     tmp = LIB + ".tmp"
-    _run(["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_o, rt_o, opt_o, "-pthread",
+    _run(["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_o, na_o, rt_o, opt_o, "-pthread",
           "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:

@@ -145,5 +145,8 @@ hipError_t sim_step_occupancy(size_t lds_bytes, int* blocks);
 // resident waves per compute unit of the first simulation kernel of a path
 hipError_t sim_occupancy(bool stepped, bool list, bool d_lds, size_t lds_bytes, int* blocks);
 hipError_t launch_finalize(const FinArgs& F, int G, hipStream_t s);
+// Device address and size of the calling thread's current device's scratch
+// array of the no-allocation entry point (svf_noalloc.hip).
+hipError_t noalloc_scratch(void** addr, size_t* bytes);
 
 }  // namespace svfk

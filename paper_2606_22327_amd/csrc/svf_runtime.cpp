@@ -7,7 +7,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
-#include <string>
+#include <mutex>
 #include <vector>
 
 #include "svf_kernels.h"
@@ -21,16 +21,16 @@ static_assert(sizeof(SegState) == 80, "state layout");
 
 namespace {
 
-thread_local std::string g_err;
+// message of the calling thread's last failure (a fixed buffer: no call
+// allocates host memory for it)
+thread_local char g_err[512];
 
 int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
 int fail(int code, const char* fmt, ...) {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
     va_end(ap);
-    g_err = buf;
     return code;
 }
 
@@ -165,12 +165,12 @@ struct HostView {
 // are done, so at most the k smallest values of s + 1 fit.  Values at or
 // above kCap count as kCap (a lower bound on each), which keeps k an upper
 // bound.
-int64_t running_bound(const int32_t* s, const std::vector<int64_t>& off, int64_t M) {
-    const int kCap = 4096;
-    std::vector<int64_t> h(kCap + 1);
+int64_t running_bound(const int32_t* s, const int64_t* off, int32_t I, int64_t M) {
+    constexpr int kCap = 4096;
+    int64_t h[kCap + 1];
     int64_t best = 0;
-    for (size_t i = 0; i + 1 < off.size(); ++i) {
-        std::fill(h.begin(), h.end(), 0);
+    for (int32_t i = 0; i < I; ++i) {
+        std::fill(h, h + kCap + 1, 0);
         for (int64_t j = off[i]; j < off[i + 1]; ++j)
             h[std::min<int64_t>((int64_t)s[j] + 1, kCap)] += 1;
         int64_t sum = 0, k = 0;
@@ -186,10 +186,10 @@ int64_t running_bound(const int32_t* s, const std::vector<int64_t>& off, int64_t
     return best;
 }
 
-// Everything that can be checked without a GPU.
-int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64_t>& off,
-             int64_t N, std::vector<uint8_t>* stepped, int64_t* max_plan, int64_t* max_profile,
-             std::vector<uint64_t>* max_key) {
+// Everything that can be checked without a GPU.  Writes each segment's path
+// (1: per-step) to stepped[P*I] and each policy's largest key to max_key[P].
+int validate(const svf_batch_desc* d, const HostView& v, const int64_t* off, int64_t N,
+             uint8_t* stepped, int64_t* max_plan, int64_t* max_profile, uint64_t* max_key) {
     const int32_t I = d->num_instances, P = d->num_policies;
     bool has1bit = false;
     for (int p = 0; p < P; ++p) has1bit |= (d->policies[p] & 0xFF) == SVF_POLICY_SVF1BIT;
@@ -202,12 +202,12 @@ int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64
     // check keeps it <= M; with next-step admission only, the requests of an
     // instance bound it together: sum of s + o^.
     *max_profile = d->M;
-    stepped->assign((size_t)P * I, 0);
-    max_key->assign(P, 0);
-    std::vector<int64_t> cur_total(P);
+    std::fill(stepped, stepped + (size_t)P * I, 0);
+    std::fill(max_key, max_key + P, 0);
+    int64_t cur_total[8];
     for (int32_t i = 0; i < I; ++i) {
         const int64_t lo = off[i], hi = off[i + 1];
-        std::fill(cur_total.begin(), cur_total.end(), 0);
+        std::fill(cur_total, cur_total + P, 0);
         for (int64_t j = lo; j < hi; ++j) {
             const int32_t a = v.a[j], s = v.s[j], o = v.o[j];
             if (a < 0 || a >= kLimit30)
@@ -240,10 +240,10 @@ int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64
                 if (key >= (uint64_t(1) << 32))
                     return fail(SVF_EINVAL, "instance %d request %lld: priority key %llu >= 2^32", i,
                                 (long long)(j - lo), (unsigned long long)key);
-                (*max_key)[p] = std::max((*max_key)[p], key);
+                max_key[p] = std::max(max_key[p], key);
                 // eviction is only possible when plans differ from the truth
                 // or when admission looks at the next step only
-                if (oh != o || current_rule) (*stepped)[(size_t)p * I + i] = 1;
+                if (oh != o || current_rule) stepped[(size_t)p * I + i] = 1;
                 *max_plan = std::max(*max_plan, oh);
                 if (current_rule) cur_total[p] += s + oh;
             }
@@ -253,7 +253,7 @@ int validate(const svf_batch_desc* d, const HostView& v, const std::vector<int64
     return SVF_OK;
 }
 
-int check_desc_shape(const svf_batch_desc* d, std::vector<int64_t>* off, int64_t* N) {
+int check_desc_shape(const svf_batch_desc* d, int64_t* N) {
     if (!d) return fail(SVF_EINVAL, "desc is NULL");
     if (d->num_instances < 0) return fail(SVF_EINVAL, "num_instances < 0");
     if (!d->req_offsets) return fail(SVF_EINVAL, "req_offsets is NULL");
@@ -269,17 +269,176 @@ int check_desc_shape(const svf_batch_desc* d, std::vector<int64_t>* off, int64_t
     if (d->M < 1 || d->M >= kLimit30) return fail(SVF_EINVAL, "M must be in [1, 2^30)");
     if (d->max_steps < 0 || d->max_steps >= kLimit30)
         return fail(SVF_EINVAL, "max_steps must be in [0, 2^30)");
-    off->assign(d->req_offsets, d->req_offsets + d->num_instances + 1);
-    if ((*off)[0] != 0) return fail(SVF_EINVAL, "req_offsets[0] must be 0");
+    const int64_t* off = d->req_offsets;
+    if (off[0] != 0) return fail(SVF_EINVAL, "req_offsets[0] must be 0");
     for (int32_t i = 0; i < d->num_instances; ++i) {
-        const int64_t n = (*off)[i + 1] - (*off)[i];
+        const int64_t n = off[i + 1] - off[i];
         if (n < 0) return fail(SVF_EINVAL, "req_offsets decreases at instance %d", i);
         if (n >= (int64_t(1) << 31) - 1)
             return fail(SVF_EINVAL, "instance %d holds too many requests", i);
     }
-    *N = (*off)[d->num_instances];
+    *N = off[d->num_instances];
     if (*N * (int64_t)d->num_policies >= (int64_t(1) << 31))
         return fail(SVF_EINVAL, "requests x policies must stay below 2^31");
+    return SVF_OK;
+}
+
+// The launch plan of a validated batch: sizes, sort shape, profile kind
+// (ring or finish-ordered list) and its LDS capacity per path, issue
+// priorities.  Fills the host fields of ``h`` (not its buffers) and the
+// bitmap word offsets bw_off[I+1].
+int plan_batch(svf_batch* h, const svf_batch_desc* d, const HostView& v, const int64_t* off,
+               const uint8_t* stepped, int64_t max_plan, int64_t max_profile,
+               const uint64_t* max_key, int64_t* bw_off) {
+    const int32_t I = d->num_instances, P = d->num_policies;
+    const int64_t N = off[I];
+    h->I = I; h->P = P; h->N = N;
+    h->M = (int32_t)d->M;
+    h->O0 = d->O0; h->O1 = d->O1;
+    h->max_steps = (int32_t)d->max_steps;
+    h->H = (int32_t)next_pow2(std::max<int64_t>(max_plan, 1));
+    for (int32_t i = 0; i < I; ++i) h->max_n = std::max<int32_t>(h->max_n, (int32_t)(off[i + 1] - off[i]));
+    h->CH = (int32_t)std::min<int64_t>(8192, std::max<int64_t>(64, next_pow2(h->max_n)));
+    h->fused_sort = h->max_n <= svfk::SORT_REC_MAX;
+    for (int32_t p = 0; p < P; ++p)
+        h->kbits[p] = max_key[p] ? 64 - __builtin_clzll(max_key[p]) : 0;
+    for (int64_t g = 0; g < (int64_t)P * I; ++g) {
+        h->any_stepped |= stepped[g] != 0;
+        (stepped[g] ? h->n_stepped : h->n_known) += 1;
+    }
+    // the profile ring stores memory + step index in int32
+    if (max_profile + h->max_steps + 2 * (int64_t)h->H >= (int64_t(1) << 31) - 1)
+        return fail(SVF_EINVAL, "M (or, under SVF_ADMIT_CURRENT, an instance's sum of s + planned "
+                                "length) + max_steps + 2 * (longest planned length, rounded up to "
+                                "a power of two) must stay below 2^31");
+
+    // bitmap word offsets of the instances
+    bw_off[0] = 0;
+    for (int32_t i = 0; i < I; ++i) {
+        const int64_t n = off[i + 1] - off[i];
+        const int64_t W0 = (n + 63) / 64, W1 = (W0 + 63) / 64;
+        bw_off[i + 1] = bw_off[i] + W0 + W1;
+        h->bw_max = std::max<int32_t>(h->bw_max, (int32_t)(W0 + W1));
+    }
+    h->bw_total = bw_off[I];
+
+    // ring placement: LDS when the ring and bitmap fit comfortably
+    const char* env = getenv("SVFSIM_RING");
+    const size_t ring_bytes = ((size_t)h->H + 64) * 4;  // H slots + spare slot
+    const size_t bm_bytes = (size_t)h->bw_max * 8;
+    h->d_lds = ring_bytes + bm_bytes <= 65536;
+    if (env && !strcmp(env, "global")) h->d_lds = false;
+    if (env && !strcmp(env, "lds") && ring_bytes + bm_bytes <= 160 * 1024) h->d_lds = true;
+    h->lds_bytes = std::max<size_t>(8, bm_bytes + (h->d_lds ? ring_bytes : 0));
+    // The event path keeps its profile as the finish-ordered list (8 bytes
+    // per running request) when the ring does not fit in LDS, or when few
+    // requests run at once: the list's checks and insertions touch the
+    // running requests that finish before the candidate, the ring's the
+    // candidate's whole planned length.  Measured: the list is faster at
+    // about 140-280 concurrent requests (4096 x 1000 and 16384 x 5000
+    // workloads), 4x slower at about 930 (64 x 200,000); the estimate is
+    // M / (mean s + mean o / 2) and the crossover is taken at 512.  The list
+    // in LDS gets the largest capacity that still lets as many waves reside
+    // as the list kernel's registers allow; segments that outgrow it stop,
+    // and a second launch with room for the bound on concurrent requests
+    // continues them.
+    const int64_t bound = (h->n_known > 0 || h->any_stepped)
+                              ? std::max<int64_t>(1, running_bound(v.s, off, I, d->M)) : 1;
+    const size_t full_bytes = bm_bytes + (size_t)svfk::list_slots((int)std::min<int64_t>(bound, 1 << 24)) * 8;
+    if (h->n_known > 0) {
+        const char* pe = getenv("SVFSIM_PROFILE");
+        bool use = false;
+        int64_t cap = bound;
+        if (full_bytes <= 160 * 1024) {
+            auto occ = [&](bool list, bool dl, size_t bytes) {
+                int w = 0;
+                return svfk::sim_known_occupancy(list, dl, bytes, &w) == hipSuccess ? w : -1;
+            };
+            const int w_top = occ(true, false, bm_bytes + (size_t)svfk::list_slots(64) * 8);
+            int64_t lo = std::min<int64_t>(bound, 64), hi = bound;  // occ(lo) >= w_top
+            while (lo < hi) {
+                const int64_t mid = lo + (hi - lo + 1) / 2;
+                if (occ(true, false, bm_bytes + (size_t)svfk::list_slots((int)mid) * 8) >= w_top) lo = mid;
+                else hi = mid - 1;
+            }
+            cap = lo;
+            const char* pc = getenv("SVFSIM_LIST_LDS_CAP");  // testing: a smaller LDS list
+            if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
+            double sum_s = 0.0, sum_o = 0.0;
+            for (int64_t x = 0; x < N; ++x) {
+                sum_s += v.s[x];
+                sum_o += v.o[x];
+            }
+            const double running = N > 0 ? (double)d->M / ((sum_s + 0.5 * sum_o) / (double)N) : 0.0;
+            if (w_top > 0) use = !h->d_lds || running <= 512.0;
+        }
+        if (pe && !strcmp(pe, "ring")) use = false;
+        if (pe && !strcmp(pe, "list")) use = full_bytes <= 160 * 1024;
+        if (use) {
+            h->list_known = true;
+            h->list_cap = (int32_t)cap;
+            h->lds_list = bm_bytes + (size_t)svfk::list_slots((int)cap) * 8;
+            h->lds_list_full = full_bytes;
+        }
+    }
+    // The per-step path keeps its planned profile as the finish-ordered list
+    // when the list with room for the bound fits in 64 KB of LDS.  As on the
+    // event path, the first launch gives it the largest capacity that keeps
+    // the kernel at the occupancy its registers allow, and a continuation
+    // launch has room for the bound.
+    if (h->any_stepped) {
+        const char* ps = getenv("SVFSIM_STEP_PROFILE");
+        bool use = full_bytes <= 64 * 1024;
+        if (ps && !strcmp(ps, "ring")) use = false;
+        if (ps && !strcmp(ps, "list")) use = full_bytes <= 160 * 1024;
+        if (use) {
+            auto occ = [&](size_t bytes) {
+                int w = 0;
+                return svfk::sim_step_occupancy(bytes, &w) == hipSuccess ? w : -1;
+            };
+            const int w_top = occ(bm_bytes + (size_t)svfk::list_slots(64) * 8);
+            int64_t lo = std::min<int64_t>(bound, 64), hi = bound;
+            while (w_top > 0 && lo < hi) {
+                const int64_t mid = lo + (hi - lo + 1) / 2;
+                if (occ(bm_bytes + (size_t)svfk::list_slots((int)mid) * 8) >= w_top) lo = mid;
+                else hi = mid - 1;
+            }
+            int64_t cap = w_top > 0 ? lo : bound;
+            const char* pc = getenv("SVFSIM_STEP_LDS_CAP");  // testing: a smaller LDS list
+            if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
+            h->list_stepped = true;
+            h->step_cap = (int32_t)cap;
+            h->lds_step = bm_bytes + (size_t)svfk::list_slots((int)cap) * 8;
+            h->lds_step_full = full_bytes;
+        }
+    }
+    if (h->list_known || h->list_stepped) h->list_stride = (int32_t)bound;
+    h->ring_used = (h->n_known > 0 && !h->list_known) || (h->any_stepped && !h->list_stepped);
+    // Resident workgroups of the first simulation launch of each path; the
+    // waves set their issue priorities only when it is known (timing only).
+    // With at most one segment per CU there is nothing to arbitrate.
+    {
+        int ncu = 0;
+        const char* pp = getenv("SVFSIM_ISSUE_PRIO");  // "0": all waves at one priority
+        const bool on = !(pp && !strcmp(pp, "0"));
+        if (on && hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess &&
+            ncu > 0 && (int64_t)P * I > ncu) {
+            int w = 0;
+            if (h->n_known > 0 &&
+                svfk::sim_occupancy(false, h->list_known, h->d_lds,
+                                    h->list_known ? h->lds_list : h->lds_bytes, &w) == hipSuccess)
+                h->res_known = w * ncu;
+            w = 0;
+            if (h->any_stepped &&
+                svfk::sim_occupancy(true, h->list_stepped, h->d_lds,
+                                    h->list_stepped ? h->lds_step : h->lds_bytes, &w) == hipSuccess)
+                h->res_stepped = w * ncu;
+        }
+        (void)hipGetLastError();
+    }
+    if (h->lds_bytes > 160 * 1024)
+        return fail(SVF_EINVAL, "an instance's rank bitmap needs %zu bytes of LDS (> 160 KB)", h->lds_bytes);
+
     return SVF_OK;
 }
 
@@ -448,22 +607,43 @@ int do_finalize(svf_batch* h) {
     return SVF_OK;
 }
 
+// Sequential placement of buffers in a fixed device region (256-byte
+// aligned); ``used`` may exceed the region, and is checked before any use.
+struct Carve {
+    char* base;
+    size_t used;
+    template <typename T>
+    T* take(int64_t count) {
+        if (count <= 0) return nullptr;
+        used = (used + 255) & ~size_t(255);
+        T* p = reinterpret_cast<T*>(base + used);
+        used += sizeof(T) * (size_t)count;
+        return p;
+    }
+};
+
+// Host tables of svf_run_noalloc (per-segment path flags, bitmap word
+// offsets), static so that the call allocates nothing; guarded by g_na_mu.
+std::mutex g_na_mu;
+uint8_t g_na_stepped[(size_t)SVF_NOALLOC_MAX_INSTANCES * 8];
+int64_t g_na_bw_off[SVF_NOALLOC_MAX_INSTANCES + 1];
+
 }  // namespace
 
 extern "C" {
 
-const char* svf_last_error(void) { return g_err.c_str(); }
+const char* svf_last_error(void) { return g_err; }
 
 int svf_abi_version(void) { return SVFSIM_ABI_VERSION; }
 
 int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
-    g_err.clear();
+    g_err[0] = 0;
     if (!out) return fail(SVF_EINVAL, "out is NULL");
     *out = nullptr;
-    std::vector<int64_t> off;
     int64_t N = 0;
-    RETCHK(check_desc_shape(d, &off, &N));
+    RETCHK(check_desc_shape(d, &N));
     const int32_t I = d->num_instances, P = d->num_policies;
+    const std::vector<int64_t> off(d->req_offsets, d->req_offsets + I + 1);
 
     // host view of the per-request arrays (device inputs are fetched first)
     std::vector<int32_t> ha, hs, ho, hp;
@@ -488,49 +668,28 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
             v.bit = hb.data();
         }
     }
-    std::vector<uint8_t> stepped;
+    std::vector<uint8_t> stepped((size_t)P * I);
     int64_t max_plan = 1, max_profile = 0;
-    std::vector<uint64_t> max_key;
-    RETCHK(validate(d, v, off, N, &stepped, &max_plan, &max_profile, &max_key));
+    uint64_t max_key[8];
+    RETCHK(validate(d, v, off.data(), N, stepped.data(), &max_plan, &max_profile, max_key));
 
     svf_batch* h = new (std::nothrow) svf_batch();
     if (!h) return fail(SVF_ENOMEM, "host allocation failed");
     h->stream = (hipStream_t)hip_stream;
     (void)hipGetDevice(&h->device);
-    h->I = I; h->P = P; h->N = N;
-    h->M = (int32_t)d->M;
-    h->O0 = d->O0; h->O1 = d->O1;
-    h->max_steps = (int32_t)d->max_steps;
     h->policies.assign(d->policies, d->policies + P);
     h->offsets = off;
-    h->H = (int32_t)next_pow2(std::max<int64_t>(max_plan, 1));
-    for (int32_t i = 0; i < I; ++i) h->max_n = std::max<int32_t>(h->max_n, (int32_t)(off[i + 1] - off[i]));
-    h->CH = (int32_t)std::min<int64_t>(8192, std::max<int64_t>(64, next_pow2(h->max_n)));
-    h->fused_sort = h->max_n <= svfk::SORT_REC_MAX;
-    for (int32_t p = 0; p < P; ++p)
-        h->kbits[p] = max_key[p] ? 64 - __builtin_clzll(max_key[p]) : 0;
-    for (uint8_t x : stepped) {
-        h->any_stepped |= x != 0;
-        (x ? h->n_stepped : h->n_known) += 1;
-    }
-    // the profile ring stores memory + step index in int32
-    if (max_profile + h->max_steps + 2 * (int64_t)h->H >= (int64_t(1) << 31) - 1) {
-        delete h;
-        return fail(SVF_EINVAL, "M (or, under SVF_ADMIT_CURRENT, an instance's sum of s + planned "
-                                "length) + max_steps + 2 * (longest planned length, rounded up to "
-                                "a power of two) must stay below 2^31");
-    }
-
-    // chunk table (segment, first position) and bitmap offsets
-    std::vector<int32_t> cseg, clo;
     std::vector<int64_t> bw_off(I + 1, 0);
-    for (int32_t i = 0; i < I; ++i) {
-        const int64_t n = off[i + 1] - off[i];
-        const int64_t W0 = (n + 63) / 64, W1 = (W0 + 63) / 64;
-        bw_off[i + 1] = bw_off[i] + W0 + W1;
-        h->bw_max = std::max<int32_t>(h->bw_max, (int32_t)(W0 + W1));
+    {
+        const int rc = plan_batch(h, d, v, off.data(), stepped.data(), max_plan, max_profile,
+                                  max_key, bw_off.data());
+        if (rc != SVF_OK) {
+            delete h;
+            return rc;
+        }
     }
-    h->bw_total = bw_off[I];
+    // chunk table (segment, first position) of the sort for large instances
+    std::vector<int32_t> cseg, clo;
     for (int32_t p = 0; p < P; ++p)
         for (int32_t i = 0; i < I; ++i) {
             const int64_t n = off[i + 1] - off[i];
@@ -540,125 +699,6 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
             }
         }
     h->nchunks = (int32_t)cseg.size();
-
-    // ring placement: LDS when the ring and bitmap fit comfortably
-    const char* env = getenv("SVFSIM_RING");
-    const size_t ring_bytes = ((size_t)h->H + 64) * 4;  // H slots + spare slot
-    const size_t bm_bytes = (size_t)h->bw_max * 8;
-    h->d_lds = ring_bytes + bm_bytes <= 65536;
-    if (env && !strcmp(env, "global")) h->d_lds = false;
-    if (env && !strcmp(env, "lds") && ring_bytes + bm_bytes <= 160 * 1024) h->d_lds = true;
-    h->lds_bytes = std::max<size_t>(8, bm_bytes + (h->d_lds ? ring_bytes : 0));
-    // The event path keeps its profile as the finish-ordered list (8 bytes
-    // per running request) when the ring does not fit in LDS, or when few
-    // requests run at once: the list's checks and insertions touch the
-    // running requests that finish before the candidate, the ring's the
-    // candidate's whole planned length.  Measured: the list is faster at
-    // about 140-280 concurrent requests (4096 x 1000 and 16384 x 5000
-    // workloads), 4x slower at about 930 (64 x 200,000); the estimate is
-    // M / (mean s + mean o / 2) and the crossover is taken at 512.  The list
-    // in LDS gets the largest capacity that still lets as many waves reside
-    // as the list kernel's registers allow; segments that outgrow it stop,
-    // and a second launch with room for the bound on concurrent requests
-    // continues them.
-    const int64_t bound = (h->n_known > 0 || h->any_stepped)
-                              ? std::max<int64_t>(1, running_bound(v.s, off, d->M)) : 1;
-    const size_t full_bytes = bm_bytes + (size_t)svfk::list_slots((int)std::min<int64_t>(bound, 1 << 24)) * 8;
-    if (h->n_known > 0) {
-        const char* pe = getenv("SVFSIM_PROFILE");
-        bool use = false;
-        int64_t cap = bound;
-        if (full_bytes <= 160 * 1024) {
-            auto occ = [&](bool list, bool dl, size_t bytes) {
-                int w = 0;
-                return svfk::sim_known_occupancy(list, dl, bytes, &w) == hipSuccess ? w : -1;
-            };
-            const int w_top = occ(true, false, bm_bytes + (size_t)svfk::list_slots(64) * 8);
-            int64_t lo = std::min<int64_t>(bound, 64), hi = bound;  // occ(lo) >= w_top
-            while (lo < hi) {
-                const int64_t mid = lo + (hi - lo + 1) / 2;
-                if (occ(true, false, bm_bytes + (size_t)svfk::list_slots((int)mid) * 8) >= w_top) lo = mid;
-                else hi = mid - 1;
-            }
-            cap = lo;
-            const char* pc = getenv("SVFSIM_LIST_LDS_CAP");  // testing: a smaller LDS list
-            if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
-            double sum_s = 0.0, sum_o = 0.0;
-            for (int64_t x = 0; x < N; ++x) {
-                sum_s += v.s[x];
-                sum_o += v.o[x];
-            }
-            const double running = N > 0 ? (double)d->M / ((sum_s + 0.5 * sum_o) / (double)N) : 0.0;
-            if (w_top > 0) use = !h->d_lds || running <= 512.0;
-        }
-        if (pe && !strcmp(pe, "ring")) use = false;
-        if (pe && !strcmp(pe, "list")) use = full_bytes <= 160 * 1024;
-        if (use) {
-            h->list_known = true;
-            h->list_cap = (int32_t)cap;
-            h->lds_list = bm_bytes + (size_t)svfk::list_slots((int)cap) * 8;
-            h->lds_list_full = full_bytes;
-        }
-    }
-    // The per-step path keeps its planned profile as the finish-ordered list
-    // when the list with room for the bound fits in 64 KB of LDS.  As on the
-    // event path, the first launch gives it the largest capacity that keeps
-    // the kernel at the occupancy its registers allow, and a continuation
-    // launch has room for the bound.
-    if (h->any_stepped) {
-        const char* ps = getenv("SVFSIM_STEP_PROFILE");
-        bool use = full_bytes <= 64 * 1024;
-        if (ps && !strcmp(ps, "ring")) use = false;
-        if (ps && !strcmp(ps, "list")) use = full_bytes <= 160 * 1024;
-        if (use) {
-            auto occ = [&](size_t bytes) {
-                int w = 0;
-                return svfk::sim_step_occupancy(bytes, &w) == hipSuccess ? w : -1;
-            };
-            const int w_top = occ(bm_bytes + (size_t)svfk::list_slots(64) * 8);
-            int64_t lo = std::min<int64_t>(bound, 64), hi = bound;
-            while (w_top > 0 && lo < hi) {
-                const int64_t mid = lo + (hi - lo + 1) / 2;
-                if (occ(bm_bytes + (size_t)svfk::list_slots((int)mid) * 8) >= w_top) lo = mid;
-                else hi = mid - 1;
-            }
-            int64_t cap = w_top > 0 ? lo : bound;
-            const char* pc = getenv("SVFSIM_STEP_LDS_CAP");  // testing: a smaller LDS list
-            if (pc && atoll(pc) > 0) cap = std::min<int64_t>(cap, atoll(pc));
-            h->list_stepped = true;
-            h->step_cap = (int32_t)cap;
-            h->lds_step = bm_bytes + (size_t)svfk::list_slots((int)cap) * 8;
-            h->lds_step_full = full_bytes;
-        }
-    }
-    if (h->list_known || h->list_stepped) h->list_stride = (int32_t)bound;
-    h->ring_used = (h->n_known > 0 && !h->list_known) || (h->any_stepped && !h->list_stepped);
-    // Resident workgroups of the first simulation launch of each path; the
-    // waves set their issue priorities only when it is known (timing only).
-    // With at most one segment per CU there is nothing to arbitrate.
-    {
-        int ncu = 0;
-        const char* pp = getenv("SVFSIM_ISSUE_PRIO");  // "0": all waves at one priority
-        const bool on = !(pp && !strcmp(pp, "0"));
-        if (on && hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, h->device) == hipSuccess &&
-            ncu > 0 && (int64_t)P * I > ncu) {
-            int w = 0;
-            if (h->n_known > 0 &&
-                svfk::sim_occupancy(false, h->list_known, h->d_lds,
-                                    h->list_known ? h->lds_list : h->lds_bytes, &w) == hipSuccess)
-                h->res_known = w * ncu;
-            w = 0;
-            if (h->any_stepped &&
-                svfk::sim_occupancy(true, h->list_stepped, h->d_lds,
-                                    h->list_stepped ? h->lds_step : h->lds_bytes, &w) == hipSuccess)
-                h->res_stepped = w * ncu;
-        }
-        (void)hipGetLastError();
-    }
-    if (h->lds_bytes > 160 * 1024) {
-        delete h;
-        return fail(SVF_EINVAL, "an instance's rank bitmap needs %zu bytes of LDS (> 160 KB)", h->lds_bytes);
-    }
 
     const int64_t G = (int64_t)P * I;
     const int64_t PN = (int64_t)P * N;
@@ -845,6 +885,106 @@ int svf_destroy(svf_batch* h) {
     (void)hipStreamSynchronize(h->stream);
     free_all(h);
     delete h;
+    return ok();
+}
+
+int svf_run_noalloc(const svf_batch_desc* d, void* hip_stream, int32_t* start, int32_t* finish,
+                    int32_t* preempt, int32_t* admit_seq, svf_instance_stats* stats) {
+    g_err[0] = 0;
+    int64_t N = 0;
+    RETCHK(check_desc_shape(d, &N));
+    const int32_t I = d->num_instances, P = d->num_policies;
+    if (d->inputs_on_device)
+        return fail(SVF_EINVAL, "svf_run_noalloc: the inputs must be host memory (inputs_on_device = 0)");
+    if (I > SVF_NOALLOC_MAX_INSTANCES)
+        return fail(SVF_EINVAL, "svf_run_noalloc: %d instances, at most %d", I,
+                    SVF_NOALLOC_MAX_INSTANCES);
+    const int64_t G = (int64_t)P * I, PN = (int64_t)P * N;
+    if (PN > 0 && (!start || !finish || !preempt || !admit_seq))
+        return fail(SVF_EINVAL, "svf_run_noalloc: an output array is NULL");
+    if (G > 0 && !stats) return fail(SVF_EINVAL, "svf_run_noalloc: stats is NULL");
+    const int64_t* off = d->req_offsets;
+    for (int32_t i = 0; i < I; ++i)
+        if (off[i + 1] - off[i] > svfk::SORT_REC_MAX)
+            return fail(SVF_EINVAL, "svf_run_noalloc: instance %d holds %lld requests, at most %d",
+                        i, (long long)(off[i + 1] - off[i]), (int)svfk::SORT_REC_MAX);
+
+    std::lock_guard<std::mutex> lock(g_na_mu);
+    const HostView v{d->arrival, d->prompt, d->output, d->plan_len, d->long_bit};
+    int64_t max_plan = 1, max_profile = 0;
+    uint64_t max_key[8];
+    RETCHK(validate(d, v, off, N, g_na_stepped, &max_plan, &max_profile, max_key));
+    svf_batch h;  // the launch plan; its buffers are the scratch and the caller's outputs
+    h.stream = (hipStream_t)hip_stream;
+    HIPCHK(hipGetDevice(&h.device));
+    RETCHK(plan_batch(&h, d, v, off, g_na_stepped, max_plan, max_profile, max_key, g_na_bw_off));
+
+    void* base = nullptr;
+    size_t cap = 0;
+    HIPCHK(svfk::noalloc_scratch(&base, &cap));
+    Carve c{static_cast<char*>(base), 0};
+    h.d_off = c.take<int64_t>(I + 1);
+    h.d_a = c.take<int32_t>(N);
+    h.d_s = c.take<int32_t>(N);
+    h.d_o = c.take<int32_t>(N);
+    if (d->plan_len) h.d_plan = c.take<int32_t>(N);
+    if (d->long_bit) h.d_bit = c.take<int8_t>(N);
+    h.d_pol = c.take<int32_t>(P);
+    h.d_rec = c.take<int4>(PN);
+    h.d_rank = c.take<int32_t>(PN);
+    h.d_stepped = c.take<uint8_t>(G);
+    h.d_bw_off = c.take<int64_t>(I + 1);
+    h.d_bitmap = c.take<uint64_t>((int64_t)P * h.bw_total);
+    if (h.ring_used) h.d_ring = c.take<int32_t>(G * (h.H + 64));
+    if (h.list_known || h.list_stepped) {
+        h.d_lst_f = c.take<int32_t>(G * (int64_t)h.list_stride);
+        h.d_lst_q = c.take<uint32_t>(G * (int64_t)h.list_stride);
+    }
+    h.d_fin = c.take<int32_t>(PN);
+    if (h.any_stepped) {
+        h.d_act = c.take<int4>(PN);
+        h.d_actkr = c.take<int2>(PN);
+        h.d_evl = c.take<int32_t>(PN);
+    }
+    h.d_st = c.take<SegState>(G);
+    h.d_prog = c.take<unsigned long long>(2);
+    if (c.used > cap)
+        return fail(SVF_EINVAL, "svf_run_noalloc: the batch needs %zu bytes of device scratch, "
+                                "more than the %zu this entry point has", c.used, cap);
+    h.d_start = start;
+    h.d_pre = preempt;
+    h.d_seq = admit_seq;
+    h.d_fin_out = finish;
+    h.d_stats = reinterpret_cast<StatsOut*>(stats);
+
+    // inputs and host tables into the scratch; everything else the call reads
+    // is rebuilt by its own kernels (the scratch keeps the previous call's data)
+    const hipMemcpyKind k = hipMemcpyHostToDevice;
+    hipError_t e = hipSuccess;
+#define CPY(dst, src, bytes) \
+    if (e == hipSuccess && (bytes) > 0) e = hipMemcpyAsync((dst), (src), (bytes), k, h.stream);
+    CPY(h.d_off, off, 8 * (I + 1));
+    CPY(h.d_a, d->arrival, 4 * N);
+    CPY(h.d_s, d->prompt, 4 * N);
+    CPY(h.d_o, d->output, 4 * N);
+    if (d->plan_len) CPY(h.d_plan, d->plan_len, 4 * N);
+    if (d->long_bit) CPY(h.d_bit, d->long_bit, N);
+    CPY(h.d_pol, d->policies, 4 * P);
+    CPY(h.d_stepped, g_na_stepped, G);
+    CPY(h.d_bw_off, g_na_bw_off, 8 * (I + 1));
+#undef CPY
+    // finishes and preemption counts start cleared, as at svf_create
+    if (e == hipSuccess) e = svfk::launch_fill_i32(h.d_fin, PN, -1, h.stream);
+    if (e == hipSuccess) e = svfk::launch_fill_i32(h.d_pre, PN, 0, h.stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h.stream);
+    if (e != hipSuccess)
+        return fail(SVF_EHIP, "svf_run_noalloc: copying the inputs failed: %s", hipGetErrorString(e));
+    HIPCHK(svfk::prepare_sim(h.d_lds, h.lds_bytes, h.list_known || h.list_stepped,
+                             std::max(h.lds_list_full, h.lds_step_full)));
+    if (h.max_n > 0) HIPCHK(svfk::prepare_sort_rec(h.max_n));
+    RETCHK(do_reset(&h));
+    RETCHK(do_sim(&h, int64_t(1) << 40));
+    RETCHK(do_finalize(&h));
     return ok();
 }
 

@@ -37,7 +37,8 @@ STATUS = {0: "done", 1: "exhausted", 2: "running"}
 # every symbol the header declares
 EXPORTS = ("svf_create", "svf_reset", "svf_step", "svf_run", "svf_read", "svf_stats",
            "svf_set_profiling", "svf_timings", "svf_shape", "svf_destroy",
-           "svf_last_error", "svf_abi_version", "svf_opt_burst", "svf_opt_burst_batch")
+           "svf_last_error", "svf_abi_version", "svf_opt_burst", "svf_opt_burst_batch",
+           "svf_run_noalloc")
 
 
 class SvfError(RuntimeError):
@@ -118,6 +119,7 @@ def load(path: str = LIB_PATH):
     lib.svf_abi_version.argtypes = []
     lib.svf_opt_burst.argtypes = [I32, V, V, I64, I64, ctypes.POINTER(I64), ctypes.POINTER(I64)]
     lib.svf_opt_burst_batch.argtypes = [I32, V, V, V, V, I64, I32, V, V, V]
+    lib.svf_run_noalloc.argtypes = [ctypes.POINTER(BatchDesc), V, V, V, V, V, V]
     for name in EXPORTS:
         if name not in ("svf_last_error",):
             getattr(lib, name).restype = ctypes.c_int
@@ -276,6 +278,60 @@ class Simulator:
 
     def __exit__(self, *exc):
         self.close()
+
+
+def run_noalloc(offsets, arrival, prompt, output, M: int, policies: Sequence[str],
+                start, finish, preempt, admit_seq, stats, plan_len=None, long_bit=None,
+                O0: int = 0, O1: int = 0, max_steps: int = 0, stream: Optional[int] = None):
+    """svf_run_noalloc: simulate to completion without any device allocation
+    by the library.  Inputs are host (numpy) arrays; ``start``, ``finish``,
+    ``preempt``, ``admit_seq`` are caller-owned contiguous int32 CUDA tensors
+    of at least num_policies * N elements (policy-slot major) and ``stats`` a
+    contiguous CUDA tensor of at least num_policies * num_instances *
+    STATS_DTYPE.itemsize bytes.  Asynchronous on ``stream`` (torch's current
+    stream by default) once the inputs are copied."""
+    lib = load()
+    keep = []
+
+    def hptr(x, dt):
+        if x is None:
+            return None
+        x = np.ascontiguousarray(x, dtype=dt)
+        keep.append(x)
+        return x.ctypes.data
+
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    pol = np.ascontiguousarray([policy_code(p) for p in policies], dtype=np.int32)
+    keep += [off, pol]
+    I, P = len(off) - 1, len(pol)
+    N = int(off[-1]) if I > 0 else 0
+    d = BatchDesc()
+    d.num_instances = I
+    d.req_offsets = off.ctypes.data
+    d.arrival = hptr(arrival, np.int32)
+    d.prompt = hptr(prompt, np.int32)
+    d.output = hptr(output, np.int32)
+    d.plan_len = hptr(plan_len, np.int32)
+    d.long_bit = hptr(long_bit, np.int8)
+    d.inputs_on_device = 0
+    d.M = int(M)
+    d.num_policies = P
+    d.policies = pol.ctypes.data
+    d.O0, d.O1 = int(O0), int(O1)
+    d.max_steps = int(max_steps)
+
+    def dptr(t, nbytes):
+        assert t.is_cuda and t.is_contiguous() and t.numel() * t.element_size() >= nbytes
+        return ctypes.c_void_p(t.data_ptr())
+
+    for t in (start, finish, preempt, admit_seq):
+        assert t.element_size() == 4
+    if stream is None:
+        stream = _current_stream()
+    _check(lib.svf_run_noalloc(ctypes.byref(d), ctypes.c_void_p(stream),
+                               dptr(start, 4 * P * N), dptr(finish, 4 * P * N),
+                               dptr(preempt, 4 * P * N), dptr(admit_seq, 4 * P * N),
+                               dptr(stats, STATS_DTYPE.itemsize * P * I)))
 
 
 def _current_stream() -> int:

@@ -130,3 +130,45 @@ def test_null_handle_calls():
         assert getattr(lib, fn)(None, *args) == -1
     assert lib.svf_read(None, 0, None, None, None, None, 0) == -1
     assert lib.svf_stats(None, 0, None) == -1
+
+
+def _noalloc_desc(n_per, instances=1, on_device=0):
+    n = n_per * instances
+    arrs = [np.zeros(n, np.int32), np.ones(n, np.int32), np.ones(n, np.int32)]
+    off = np.arange(instances + 1, dtype=np.int64) * n_per
+    pol = np.array([2], dtype=np.int32)
+    d = S.BatchDesc()
+    d.num_instances = instances
+    d.req_offsets = off.ctypes.data
+    d.arrival, d.prompt, d.output = (a.ctypes.data for a in arrs)
+    d.M = 100
+    d.num_policies = 1
+    d.policies = pol.ctypes.data
+    d.max_steps = 10 ** 6
+    d.inputs_on_device = on_device
+    return d, (arrs, off, pol)
+
+
+def test_noalloc_rejects_bad_calls_before_touching_the_gpu():
+    """svf_run_noalloc's limits and argument checks come before any HIP call:
+    instances over 8192 requests, more than SVF_NOALLOC_MAX_INSTANCES
+    instances, device inputs, NULL outputs."""
+    import ctypes
+
+    lib = S.load()
+    src = open(HEADER).read()
+    assert int(re.search(r"SVF_NOALLOC_MAX_INSTANCES\s+(\d+)", src).group(1)) == 65536
+    assert re.search(r"SVF_NOALLOC_SCRATCH_BYTES\s+\(128u << 20\)", src)
+    buf = np.zeros(16, np.int32)
+    p = ctypes.c_void_p(buf.ctypes.data)
+    cases = [(_noalloc_desc(8193), "at most 8192"),
+             (_noalloc_desc(1, instances=65537), "at most 65536"),
+             (_noalloc_desc(4, on_device=1), "host memory")]
+    for (d, keep), msg in cases:
+        rc = lib.svf_run_noalloc(ctypes.byref(d), None, p, p, p, p, p)
+        assert rc == -1 and msg in S.last_error(), (rc, S.last_error())
+    d, keep = _noalloc_desc(4)
+    assert lib.svf_run_noalloc(ctypes.byref(d), None, None, p, p, p, p) == -1
+    assert "NULL" in S.last_error()
+    assert lib.svf_run_noalloc(ctypes.byref(d), None, p, p, p, p, None) == -1
+    assert lib.svf_run_noalloc(None, None, p, p, p, p, p) == -1
