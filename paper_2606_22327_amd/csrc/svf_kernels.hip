@@ -1544,14 +1544,17 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
             load_arrivals(cursor);
         }
         lds_order();
-        // 2. completions and requests reaching their planned length: a group
-        //    of up to 256 entries is read at once, then compacted in place
-        //    (kept entries only move to lower slots)
+        // 2. completions and requests reaching their planned length: groups
+        //    of up to 256 entries are read at once.  The list's order does
+        //    not matter (evictions choose by volume, then index), so the
+        //    entries that leave are replaced by the entries that stay from
+        //    the end of the list: one move per hole instead of shifting
+        //    everything behind the first one.
         if (nA > 0 && t >= next_ev) {
-            int newA = 0;
             int64_t dC = 0;
             int dN = 0, dfin = 0;
             int nxt = INT32_MAX;  // next event of the entries that stay
+            int rem = 0;          // lane i: position of the i-th entry that leaves (first 64)
             for (int base = 0; base < nA; base += 256) {
                 int4 qq[4];
                 int2 kr[4];
@@ -1579,13 +1582,8 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                         }
                         if (!done) nxt = min(nxt, (e < oh && oh < o) ? k + oh : k + o);
                     }
-                    const uint64_t dm = ballot(done);
-                    if (dm == 0ull) {  // nothing leaves: entries stay (or move down)
-                        const int pos = newA + lane;
-                        if (live && pos != x) { A.q[pos] = qq[u]; A.kr[pos] = kr[u]; }
-                        newA += __popcll(ballot(live));
-                        continue;
-                    }
+                    uint64_t dm = ballot(done);
+                    if (dm == 0ull) continue;
                     // early finishers give back their planned future
                     uint64_t early = ballot(done && oh > o);
                     while (early) {
@@ -1594,14 +1592,59 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                         D.remove(t, __builtin_amdgcn_readlane(s, src), __builtin_amdgcn_readlane(k, src),
                                  __builtin_amdgcn_readlane(oh, src));
                     }
-                    const uint64_t keep = ballot(live && !done);
-                    dfin += __popcll(dm);
-                    const int pos = newA + __popcll(keep & ((1ull << lane) - 1ull));
-                    if (live && !done) {
-                        A.q[pos] = qq[u];
-                        A.kr[pos] = kr[u];
+                    while (dm) {
+                        const int b = __builtin_ctzll(dm);
+                        dm &= dm - 1;
+                        if (lane == dfin) rem = base + 64 * u + b;
+                        ++dfin;
                     }
-                    newA += __popcll(keep);
+                }
+            }
+            const int newA = nA - dfin;
+            if (dfin > 64) {
+                // many at once: compact in place, keeping the order (an
+                // entry's place only moves down, after its group was read)
+                int pos0 = 0;
+                for (int base = 0; base < nA; base += 256) {
+                    int4 qq[4];
+                    int2 kr[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int x = min(base + 64 * u + lane, nA - 1);
+                        qq[u] = A.q[x];
+                        kr[u] = A.kr[x];
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int x = base + 64 * u + lane;
+                        const bool stay = x < nA && t - kr[u].x != qq[u].w;
+                        const uint64_t keep = ballot(stay);
+                        const int pos = pos0 + __popcll(keep & ((1ull << lane) - 1ull));
+                        if (stay && pos != x) {
+                            A.q[pos] = qq[u];
+                            A.kr[pos] = kr[u];
+                        }
+                        pos0 += __popcll(keep);
+                    }
+                }
+            } else if (dfin > 0) {
+                // holes: the positions that left below newA (the first h, in
+                // order); the entries that stay at or above newA fill them
+                const int h = (int)__popcll(ballot(lane < dfin && rem < newA));
+                uint64_t gone = 0ull;  // positions newA + j that left
+                for (int i = h; i < dfin; ++i)
+                    gone |= 1ull << (__builtin_amdgcn_readlane(rem, i) - newA);
+                uint64_t stay = ~gone & (dfin == 64 ? ~0ull : ((1ull << dfin) - 1ull));
+                int src = 0;
+                for (int i = 0; i < h; ++i) {
+                    if (lane == i) src = newA + __builtin_ctzll(stay);
+                    stay &= stay - 1ull;
+                }
+                if (lane < h) {
+                    const int4 mq = A.q[src];
+                    const int2 mk = A.kr[src];
+                    A.q[rem] = mq;
+                    A.kr[rem] = mk;
                 }
             }
             nA = uni(newA);
@@ -1621,8 +1664,12 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
         {
             int64_t mem_next = planned_next() + C_O + (int64_t)N_O * (t + 1);
             while (mem_next > M && nA > 0) {
+                // the scan keeps each lane's best entry and the list's last
+                // entry in registers: no load after it
                 long long bestR = -1;
                 int bestIdx = -1, bestPos = -1;
+                int4 bq = make_int4(0, 0, 0, 0), lq = make_int4(0, 0, 0, 0);
+                int2 bkr = make_int2(0, 0), lkr = make_int2(0, 0);
                 for (int base = 0; base < nA; base += 256) {
                     int4 qq[4];
                     int2 kr[4];
@@ -1643,6 +1690,12 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                             bestR = R;
                             bestIdx = qq[u].x;
                             bestPos = x;
+                            bq = qq[u];
+                            bkr = kr[u];
+                        }
+                        if (x == nA - 1) {
+                            lq = qq[u];
+                            lkr = kr[u];
                         }
                     }
                 }
@@ -1651,15 +1704,20 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                 const uint64_t who = ballot(bestR == gR && bestIdx == gIdx);
                 const int src = __builtin_ctzll(who);
                 const int vpos = __builtin_amdgcn_readlane(bestPos, src);
-                const int4 q = A.q[vpos];
-                const int2 vkr = A.kr[vpos];
+                const int4 q = readlane4(bq, src);
+                const int2 vkr = make_int2(__builtin_amdgcn_readlane(bkr.x, src),
+                                           __builtin_amdgcn_readlane(bkr.y, src));
+                const int lsrc = (nA - 1) & 63;
+                const int4 last_q = readlane4(lq, lsrc);
+                const int2 last_kr = make_int2(__builtin_amdgcn_readlane(lkr.x, lsrc),
+                                               __builtin_amdgcn_readlane(lkr.y, lsrc));
                 const int k = vkr.x;
                 const int e = t - k;
                 if (e < q.z) D.remove(t, q.y, k, q.z);
                 else { C_O -= (int64_t)(q.y - k); N_O -= 1; }
                 if (lane == 0) {
-                    A.q[vpos] = A.q[nA - 1];
-                    A.kr[vpos] = A.kr[nA - 1];
+                    A.q[vpos] = last_q;
+                    A.kr[vpos] = last_kr;
                     sg.preempt[q.x] += 1;
                     sg.start[q.x] = -1;
                     sg.admit_seq[q.x] = -1;

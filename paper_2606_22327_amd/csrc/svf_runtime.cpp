@@ -53,6 +53,11 @@ struct Timed {
 
 struct svf_batch {
     hipStream_t stream = nullptr;
+    // Second stream (default priority) on which the per-step segments run
+    // concurrently with the event-driven ones, forked from and joined back
+    // into ``stream`` with events; null: both launches on ``stream``.
+    hipStream_t aux = nullptr;
+    hipEvent_t fork_ev = nullptr, join_ev = nullptr;
     int device = 0;
     int32_t I = 0, P = 0;
     int64_t N = 0;
@@ -139,6 +144,11 @@ void free_all(svf_batch* h) {
         (void)hipEventDestroy(t.b);
     }
     h->timed.clear();
+    if (h->fork_ev) (void)hipEventDestroy(h->fork_ev);
+    if (h->join_ev) (void)hipEventDestroy(h->join_ev);
+    if (h->aux) (void)hipStreamDestroy(h->aux);
+    h->fork_ev = h->join_ev = nullptr;
+    h->aux = nullptr;
 }
 
 #define HIPCHK(expr)                                                                  \
@@ -552,31 +562,51 @@ int do_sim(svf_batch* h, int64_t delta) {
     HIPCHK(svfk::launch_fill_u64(reinterpret_cast<uint64_t*>(h->d_prog), 2, 0ull, h->stream));
     hipEvent_t e0 = nullptr;
     record(h, 1, &e0);
+    // The two paths simulate disjoint segments (each kernel leaves the other
+    // path's segments alone) and keep separate progress counters, so with
+    // segments on both the event-driven launch runs on the second stream,
+    // concurrently with the per-step one.  The per-step launch (long serial
+    // segments at low occupancy) goes first, on the caller's stream, so that
+    // its waves are resident from the start; the event-driven waves fill the
+    // remaining slots.
+    const bool fork = h->aux && h->n_known > 0 && h->n_stepped > 0;
+    const hipStream_t st_stepped = h->stream;
+    hipStream_t st_known = h->stream;
+    if (fork) {
+        HIPCHK(hipEventRecord(h->fork_ev, h->stream));
+        HIPCHK(hipStreamWaitEvent(h->aux, h->fork_ev, 0));
+        st_known = h->aux;
+    }
+    if (h->n_stepped > 0) {
+        svfk::SimArgs T = S;
+        T.list_cap = h->step_cap;
+        T.list_resume = 0;
+        T.resident = h->res_stepped;
+        T.prog = h->d_prog + 1;
+        HIPCHK(svfk::launch_sim(T, G, h->d_lds, true, h->list_stepped,
+                                h->list_stepped ? h->lds_step : h->lds_bytes, st_stepped));
+        if (h->list_stepped && h->step_cap < h->list_stride) {
+            // segments whose list outgrew the LDS capacity, up to the same step
+            T.list_cap = h->list_stride;
+            T.list_resume = 1;
+            T.resident = 0;
+            HIPCHK(svfk::launch_sim(T, G, false, true, true, h->lds_step_full, st_stepped));
+        }
+    }
     if (h->n_known > 0) {
         HIPCHK(svfk::launch_sim(S, G, h->d_lds, false, h->list_known,
-                                h->list_known ? h->lds_list : h->lds_bytes, h->stream));
+                                h->list_known ? h->lds_list : h->lds_bytes, st_known));
         if (h->list_known && h->list_cap < h->list_stride) {
             // segments whose list outgrew the LDS capacity, up to the same step
             S.list_cap = h->list_stride;
             S.list_resume = 1;
             S.resident = 0;
-            HIPCHK(svfk::launch_sim(S, G, false, false, true, h->lds_list_full, h->stream));
+            HIPCHK(svfk::launch_sim(S, G, false, false, true, h->lds_list_full, st_known));
         }
     }
-    if (h->n_stepped > 0) {
-        S.list_cap = h->step_cap;
-        S.list_resume = 0;
-        S.resident = h->res_stepped;
-        S.prog = h->d_prog + 1;
-        HIPCHK(svfk::launch_sim(S, G, h->d_lds, true, h->list_stepped,
-                                h->list_stepped ? h->lds_step : h->lds_bytes, h->stream));
-        if (h->list_stepped && h->step_cap < h->list_stride) {
-            // segments whose list outgrew the LDS capacity, up to the same step
-            S.list_cap = h->list_stride;
-            S.list_resume = 1;
-            S.resident = 0;
-            HIPCHK(svfk::launch_sim(S, G, false, true, true, h->lds_step_full, h->stream));
-        }
+    if (fork) {
+        HIPCHK(hipEventRecord(h->join_ev, h->aux));
+        HIPCHK(hipStreamWaitEvent(h->stream, h->join_ev, 0));
     }
     record_end(h, 1, e0);
     h->sim_launches += 1;
@@ -777,6 +807,14 @@ int svf_create(const svf_batch_desc* d, void* hip_stream, svf_batch** out) {
     if (e == hipSuccess && h->fused_sort) {
         hipError_t a = svfk::prepare_sort_rec(h->max_n);
         if (a != hipSuccess) e = a;
+    }
+    // both paths in one batch: a second stream for the per-step launches
+    // (SVFSIM_CONCURRENT=0 keeps them on one stream)
+    const char* pc = getenv("SVFSIM_CONCURRENT");
+    if (e == hipSuccess && h->n_known > 0 && h->n_stepped > 0 && !(pc && !strcmp(pc, "0"))) {
+        e = hipStreamCreateWithFlags(&h->aux, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&h->fork_ev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&h->join_ev, hipEventDisableTiming);
     }
     if (e != hipSuccess) {
         free_all(h);
