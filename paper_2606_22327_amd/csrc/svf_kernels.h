@@ -73,8 +73,6 @@ struct SortArgs {
 struct SimArgs {
     const int64_t* offsets;
     const int32_t* a;
-    const int32_t* s;         // [N] prompt sizes and true lengths, index order (the
-    const int32_t* o;         //   event path's arrivals read their records from them)
     const int4* rec;
     const int32_t* rank;
     const uint8_t* stepped;   // [G] 1: per-step path (plans differ or next-step admission)

@@ -416,8 +416,6 @@ struct Seg {
     const int4* __restrict__ rec;
     const int32_t* __restrict__ rank;
     const int32_t* __restrict__ a;
-    const int32_t* __restrict__ s;   // prompt sizes and true lengths, index order
-    const int32_t* __restrict__ o;
     int32_t* __restrict__ start;
     int32_t* __restrict__ fin;
     int32_t* __restrict__ preempt;
@@ -1069,9 +1067,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
     int max_fin = uni(st.max_fin), head = uni(st.head_rank), t_f = uni(st.t_f);
     int status = STATUS_RUNNING;
 
-    // Arrival window: lane l holds request wb + l (arrival, rank, record).  On
-    // this path the planned length is the true one, so the record {index, s,
-    // o^, o} comes from the index-ordered inputs, read coalesced.
+    // Arrival window: lane l holds request wb + l (arrival, rank, record).
     int wb = 0, a_reg = INT32_MAX, rk_reg = 0;
     int4 aq = make_int4(0, 0, 0, 0);
     auto load_arrivals = [&](int base) {
@@ -1083,8 +1079,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
             a_reg = sg.a[i];
             rk_reg = sg.rank[i];
             if ((unsigned)rk_reg >= (unsigned)n) rk_reg = 0;  // only a broken sort
-            const int o = sg.o[i];
-            aq = make_int4(i, sg.s[i], o, o);
+            aq = sg.rec[rk_reg];
         }
     };
     load_arrivals(cursor);
@@ -1905,8 +1900,6 @@ __device__ __forceinline__ void sim_segment(const SimArgs& P) {
     sg.rec = P.rec + base;
     sg.rank = P.rank + base;
     sg.a = P.a + off;
-    sg.s = P.s + off;
-    sg.o = P.o + off;
     sg.start = P.start + base;
     sg.fin = P.fin + base;
     sg.preempt = P.preempt + base;

@@ -530,8 +530,6 @@ int do_sim(svf_batch* h, int64_t delta) {
     svfk::SimArgs S{};
     S.offsets = h->d_off;
     S.a = h->d_a;
-    S.s = h->d_s;
-    S.o = h->d_o;
     S.rec = h->d_rec;
     S.rank = h->d_rank;
     S.stepped = h->d_stepped;
