@@ -1,8 +1,9 @@
 """The no-allocation entry point (svf_run_noalloc) against the handle-based
 entry points (svf_create + svf_run + svf_read + svf_stats) on the same
 batches: every per-request output and every per-instance statistic must be
-identical.  Calls come in a row on one GPU, each smaller than the one before,
-so that each must clear what the previous call left in the shared scratch."""
+identical.  Calls come in a row on one GPU, the later ones smaller than the
+ones before, so that each must clear what the previous call left in the
+shared scratch."""
 
 import numpy as np
 import pytest
@@ -59,6 +60,10 @@ def assert_same(b, pols, label):
 
 
 def test_noalloc_equals_the_handle_entry_points_on_calls_in_a_row():
+    # 0: the large-queue shape (event path with the ring profile in LDS)
+    b5 = W.config(5, instances=2, n=6000, burst=1500)
+    print(f"[noalloc] call 0: config 5 reduced, {b5.num_requests} requests", flush=True)
+    assert_same(b5, b5.policies, "cfg5")
     # 1: the 1-bit workload (per-step path with evictions, and the event path)
     b3 = W.config(3, instances=24, n=600)
     print(f"[noalloc] call 1: config 3 reduced, {b3.num_requests} requests x "
