@@ -549,6 +549,22 @@ def test_stepped_jumps_across_launch_limits(kw):
         compare(b, whole[pol], pol, label=f"jumps{kw}")
 
 
+def test_concurrent_launches_equal_one_stream(monkeypatch):
+    """A batch with event-driven and per-step segments runs its two launches on
+    two streams; on one stream (SVFSIM_CONCURRENT=0) every output is the same,
+    and both equal the oracle on sampled instances."""
+    b = W.config(3, instances=64, n=500)
+    say("concurrent launches vs one stream")
+    two = gpu_run(b)
+    monkeypatch.setenv("SVFSIM_CONCURRENT", "0")
+    one = gpu_run(b)
+    for pol in b.policies:
+        for f in FIELDS:
+            assert np.array_equal(two[pol][f], one[pol][f]), (pol, f)
+        assert np.array_equal(two[pol]["stats"], one[pol]["stats"]), pol
+        compare(b, two[pol], pol, ids=_sample(b.num_instances, 8, 11), label="concurrent")
+
+
 def test_issue_priorities_do_not_change_results(monkeypatch):
     """More segments than the GPU holds at once (several rounds of resident
     workgroups), on the event and the per-step path: outputs with the waves'
