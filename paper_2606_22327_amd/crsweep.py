@@ -8,12 +8,18 @@ simulated on the GPU under SVF, SJF and FCFS in one batch per alpha, and their
 exact optima come from the host solver of ``svfopt.h`` (branch and bound over
 the integer program of Section 3.1).
 
-Two modes:
+Three modes:
   sweep   random instances at each alpha (``workloads.tiny_alpha_instances``);
   search  an evolutionary search for instances with a large SVF / OPT ratio:
           every generation mutates each member once, evaluates all children in
           one GPU batch and one threaded optimum pass, and keeps the worse
-          (higher-ratio) of parent and child.
+          (higher-ratio) of parent and child;
+  bound   instances of hundreds to thousands of requests, too large for an
+          exact optimum, measured against the lower bound of the optimum that
+          the competitive-ratio proof uses (``opt_lower_bound``): TEL / LB is
+          an upper estimate of TEL / OPT.  At small alpha a tiny instance fits
+          in memory at once and every policy is optimal; these instances keep
+          the memory contended at alpha = 1/10, 1/20, 1/100.
 
 Run ``python -m paper_2606_22327_amd.crsweep`` (GPU).
 """
@@ -78,6 +84,57 @@ def evaluate(batch, threads: int = 0):
     if (st != 0).any():
         raise RuntimeError(f"optimum not found for {int((st != 0).sum())} instances")
     return tel, opt, gpu_ms, opt_s, int(states.sum())
+
+
+def opt_lower_bound(prompt, output, M: int) -> int:
+    """Lower bound on the optimal total latency of a burst instance: the
+    larger of the area bound of Proposition prop:opt_lower_bound (the volumes
+    of Eq. 1 in ascending order v_1 <= ... <= v_n; M * TEL(OPT) >=
+    sum_j sum_{i <= j} v_i) and Lemma lemma:opt_lb_execution (a request
+    cannot finish before o_i steps: TEL(OPT) >= sum_i o_i)."""
+    s = np.asarray(prompt, dtype=np.int64)
+    o = np.asarray(output, dtype=np.int64)
+    v = np.sort(s * o + (o * o + o) // 2)
+    n = len(v)
+    # sum_j sum_{i <= j} v_i = sum_i v_i (n - i), i counted from 0
+    area = int((v * (n - np.arange(n, dtype=np.int64))).sum())
+    return max(-(-area // int(M)), int(o.sum()))
+
+
+def simulate_tel(batch):
+    """Total latency of every policy per instance (GPU)."""
+    from . import svfsim as S
+
+    sim = S.Simulator.from_batch(batch, POLICIES)
+    try:
+        sim.set_profiling(True)
+        sim.reset()
+        sim.run()
+        stats = {p: sim.stats(j) for j, p in enumerate(POLICIES)}
+        gpu_ms = sim.timings()["sim_ms"]
+    finally:
+        sim.close()
+    for p in POLICIES:
+        if (stats[p]["status"] != 0).any():
+            raise RuntimeError(f"{p}: an instance did not finish")
+    return {p: stats[p]["sum_latency"].astype(np.int64) for p in POLICIES}, gpu_ms
+
+
+def bound_sweep(ks: Sequence[int], count: int, n: int, s_max: int = 32, o_max: int = 32,
+                tag: int = 0) -> List[Result]:
+    """Burst instances of n requests at alpha = 1/k (request 0 the largest,
+    M = k (s_max + o_max)) under every policy on the GPU; the ratios are total
+    latency over ``opt_lower_bound``."""
+    from . import workloads as W
+
+    out = []
+    for k in ks:
+        b = W.tiny_alpha_instances(k, count, n, n, s_max, o_max, tag=2000 + tag)
+        tel, gpu_ms = simulate_tel(b)
+        lb = np.array([opt_lower_bound(b.instance(i)["prompt"], b.instance(i)["output"], b.M)
+                       for i in range(b.num_instances)], dtype=np.int64)
+        out.append(_summarise(k, b, tel, lb, gpu_ms, 0.0, 0))
+    return out
 
 
 def _summarise(k, batch, tel, opt, gpu_ms, opt_s, states) -> Result:
@@ -180,6 +237,10 @@ def main(argv=None):
                     help="alpha values searched (at larger k every tiny instance fits at once)")
     ap.add_argument("--population", type=int, default=512)
     ap.add_argument("--threads", type=int, default=0)
+    ap.add_argument("--bound-n", type=int, default=2000,
+                    help="requests per instance of the lower-bound mode (0: skip it)")
+    ap.add_argument("--bound-count", type=int, default=256)
+    ap.add_argument("--bound-k", default="2,4,10,20,100")
     ap.add_argument("--json", action="store_true")
     args = ap.parse_args(argv)
     ks = [int(x) for x in args.k.split(",")]
@@ -190,6 +251,12 @@ def main(argv=None):
     t0 = time.perf_counter()
     rows = sweep(ks, args.count, n_hi=args.n_max, threads=args.threads)
     log(f"sweep done in {time.perf_counter() - t0:.1f}s")
+    brows = []
+    if args.bound_n > 0:
+        t0 = time.perf_counter()
+        brows = bound_sweep([int(x) for x in args.bound_k.split(",")], args.bound_count,
+                            args.bound_n)
+        log(f"lower-bound sweep done in {time.perf_counter() - t0:.1f}s")
     found = []
     if args.search_generations > 0:
         for k in [int(x) for x in args.search_k.split(",")]:
@@ -198,8 +265,13 @@ def main(argv=None):
     if args.json:
         for r in rows + found:
             print(json.dumps(r.__dict__))
+        for r in brows:
+            print(json.dumps(dict(r.__dict__, mode="lower-bound", n=args.bound_n)))
     else:
         print(table(rows, f"random burst instances (n in 6..{args.n_max}, s <= 4, o <= 6)"))
+        if brows:
+            print(table(brows, f"n = {args.bound_n} requests, s and o <= 32: total latency over "
+                               "the optimum's lower bound (an upper estimate of the ratio)"))
         if found:
             print(table(found, "after the evolutionary search for a large SVF / OPT ratio"))
             for r in found:

@@ -84,3 +84,37 @@ def test_alpha_instances_and_bound_table():
         a = int(num) / int(den)
         assert CR.cr_bound(a) == pytest.approx(bounds.cr_bound(a))
         assert round(CR.cr_bound(a), 2) == pytest.approx(float(printed))
+
+
+def test_opt_lower_bound_matches_the_paper_and_the_optimum():
+    """crsweep.opt_lower_bound is max(area bound of Proposition
+    prop:opt_lower_bound, sum o of Lemma lemma:opt_lb_execution): equal to
+    the oracle's own implementation of each on random instances, and never
+    above the exact optimum of tiny instances."""
+    from oracle import bounds, opt as oopt
+    from paper_2606_22327_amd import crsweep
+
+    rng = np.random.default_rng(17)
+    for _ in range(200):
+        n = int(rng.integers(1, 60))
+        s = rng.integers(1, 50, n)
+        o = rng.integers(1, 50, n)
+        M = int((s + o).max()) * int(rng.integers(1, 20))
+        want = max(-(-bounds.opt_lower_bound_area(s, o, M) // M), bounds.opt_lower_bound_exec(o))
+        assert crsweep.opt_lower_bound(s, o, M) == want
+    for inst in W.tiny_cr_instances(60):
+        M = int(inst["M"])
+        lb = crsweep.opt_lower_bound(inst["prompt"], inst["output"], M)
+        assert lb <= oopt.optimal_total_latency(inst["prompt"], inst["output"], M)
+
+
+@pytest.mark.gpu
+def test_lower_bound_sweep_small():
+    from paper_2606_22327_amd import crsweep
+
+    rows = crsweep.bound_sweep([2, 10], count=16, n=200)
+    for r in rows:
+        for p in crsweep.POLICIES:
+            assert r.mean_ratio[p] >= 1.0 and r.max_ratio[p] >= r.mean_ratio[p]
+        # the proof of thm:svf-burst bounds SVF by these same lower bounds
+        assert r.max_ratio["svf"] <= r.bound
