@@ -225,10 +225,12 @@ def main():
     # results of the last step
     req_steps = 0
     status_ok = True
+    inst_steps = []
     for slot in range(len(batch.policies)):
         st = sim.stats(slot)
         req_steps += int(st["request_steps"].sum())
         status_ok &= bool((st["status"] == 0).all())
+        inst_steps.append(st["t_end"].astype(np.float64))
     sim.close()
     ms_per_step = wall * 1000.0 / args.steps
     value = req_steps / (ms_per_step / 1000.0)
@@ -296,7 +298,11 @@ def main():
                    "instances": batch.num_instances,
                    "requests": batch.num_requests, "policies": list(batch.policies),
                    "M": batch.M, "request_steps_per_step": req_steps,
-                   "all_instances_done": status_ok},
+                   "all_instances_done": status_ok,
+                   # simulated steps per instance (its last step) and their
+                   # rate within the simulation launch
+                   "instance_steps_mean": float(np.mean(np.concatenate(inst_steps))),
+                   "instance_steps_per_s": float(np.mean(np.concatenate(inst_steps))) / sim_avg_s},
         "roofline": roof,
         "kernel_ms": {"init": tm["init_ms"] / args.steps, "sim": tm["sim_ms"] / args.steps,
                       "final": tm["final_ms"] / args.steps},
