@@ -192,7 +192,8 @@ def main():
         f"in {time.perf_counter() - t0:.1f}s")
     t0 = time.perf_counter()
     sim = S.Simulator.from_batch(batch)
-    log(f"created handle (inputs copied to HBM) in {time.perf_counter() - t0:.1f}s")
+    create_s = time.perf_counter() - t0
+    log(f"created handle (inputs copied to HBM) in {create_s:.1f}s")
 
     def one_step():
         sim.reset()
@@ -231,7 +232,15 @@ def main():
         req_steps += int(st["request_steps"].sum())
         status_ok &= bool((st["status"] == 0).all())
         inst_steps.append(st["t_end"].astype(np.float64))
+    # outputs back to host memory (outside the timed region)
+    t0 = time.perf_counter()
+    out_bytes = 0
+    for slot in range(len(batch.policies)):
+        out_bytes += sum(a.nbytes for a in sim.read(slot).values())
+    read_s = time.perf_counter() - t0
     sim.close()
+    in_bytes = sum(a.nbytes for a in (batch.offsets, batch.arrival, batch.prompt, batch.output,
+                                      batch.plan_len, batch.long_bit) if a is not None)
     ms_per_step = wall * 1000.0 / args.steps
     value = req_steps / (ms_per_step / 1000.0)
 
@@ -306,6 +315,12 @@ def main():
         "roofline": roof,
         "kernel_ms": {"init": tm["init_ms"] / args.steps, "sim": tm["sim_ms"] / args.steps,
                       "final": tm["final_ms"] / args.steps},
+        # host buffers in and out, never part of value: svf_create (host
+        # validation, launch plan, inputs to HBM) and svf_read of every output
+        "host_io": {"create_s": create_s, "input_bytes": int(in_bytes), "read_s": read_s,
+                    "output_bytes": int(out_bytes),
+                    "request_steps_per_s_with_host_io":
+                        req_steps / (create_s + ms_per_step / 1000.0 + read_s)},
     }
     if not args.no_cpu_baseline:
         # one GPU's share of the host is 16 cores: at most 16 oracle threads
