@@ -442,6 +442,52 @@ def test_degenerate_cases():
         assert np.array_equal(g[pol]["start"], b2.arrival)
 
 
+def _parts_near_largest_budget(seed, instances, M, plans):
+    """Four requests at t = 0 whose prompts nearly fill M (slack of 0..63
+    tokens, so that a few steps of growth overflow it) and three smaller later
+    arrivals; lengths 1..12, plans 1..4 when asked for."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    parts = []
+    for _ in range(instances):
+        base = (M - int(rng.integers(0, 64))) // 4
+        s = np.concatenate([base + rng.integers(-3, 4, 4), rng.integers(2 ** 18, 2 ** 26, 3)])
+        a = np.concatenate([np.zeros(4, np.int64), np.sort(rng.integers(0, 20, 3))])
+        o = rng.integers(1, 13, 7)
+        d = {"arrival": a, "prompt": s, "output": o, "long_bit": (o > 4).astype(np.int8)}
+        if plans:
+            d["plan_len"] = rng.integers(1, 5, 7)
+        parts.append(d)
+    return parts
+
+
+@pytest.mark.parametrize("profile", ["ring", "list"])
+def test_largest_memory_budget(profile):
+    """M = 2^30 - 1, the largest budget the library accepts, with prompts of
+    up to 2^28 tokens: every memory total, planned sum and release step sits
+    near the top of the int32 range.  Known lengths, 1-bit plans, noisy plans
+    and next-step admission (evictions included), each profile forced."""
+    M = 2 ** 30 - 1
+    os.environ["SVFSIM_PROFILE"] = profile
+    os.environ["SVFSIM_STEP_PROFILE"] = profile
+    try:
+        for plans, pols in ((False, ("svf", "sjf", "fcfs", "svf1bit", "svf+cur", "fcfs+cur",
+                                     "svf1bit+cur")),
+                            (True, ("svf", "sjf", "svf+cur"))):
+            b = W.assemble("budget", _parts_near_largest_budget(11, 48, M, plans), M, pols,
+                           O0=2, O1=8)
+            say(f"largest budget, {profile}, plans={plans}")
+            g = gpu_run(b)
+            evicted = 0
+            for pol in pols:
+                compare(b, g[pol], pol, label=f"budget-{profile}")
+                assert int(g[pol]["stats"]["peak_mem"].max()) > M - 64
+                evicted += int(g[pol]["preempt"].sum())
+            assert evicted > 0, "no eviction near the budget"
+    finally:
+        del os.environ["SVFSIM_PROFILE"]
+        del os.environ["SVFSIM_STEP_PROFILE"]
+
+
 def test_step_by_step_equals_run_and_partial_states():
     b = W.random_small(11, instances=24, n_max=50, s_max=10, o_max=16, M=40, gap_mean=0.5,
                        bits=True)
