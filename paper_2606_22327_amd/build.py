@@ -51,6 +51,38 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# The runtime's host code under the address and undefined-behaviour
+# sanitizers (device code is not instrumented: each flag goes to the host
+# compilation only), for the ABI test driver of tests/native.
+SAN_HOST = ["-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-sanitize-recover=all",
+            "-Xarch_host", "-fno-omit-frame-pointer"]
+SAN_EXE = os.path.join(BUILD, "abi_asan")
+
+
+def build_abi_sanitized(verbose: bool = False) -> str:
+    """Link tests/native/abi_asan_main.cpp and a sanitized build of the
+    runtime with the kernel objects of ``build()`` into ``_build/abi_asan``."""
+    kern_o = os.path.join(BUILD, "svf_kernels.o")
+    na_o = os.path.join(BUILD, "svf_noalloc.o")
+    if not (os.path.exists(kern_o) and os.path.exists(na_o)):
+        build()
+    flags = ["-O1", "-g", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
+    rt_o = os.path.join(BUILD, "svf_runtime_san.o")
+    drv_o = os.path.join(BUILD, "abi_asan_main.o")
+    _run(["hipcc", *flags, *SAN_HOST, "-c", os.path.join(CSRC, "svf_runtime.cpp"), "-o", rt_o])
+    _run(["hipcc", *flags, *SAN_HOST, "-c", os.path.join(ROOT, "tests", "native", "abi_asan_main.cpp"),
+          "-o", drv_o])
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    tmp = SAN_EXE + ".tmp"
+    _run([os.path.join(rocm, "llvm", "bin", "clang++"), "-fsanitize=address,undefined", drv_o, rt_o,
+          kern_o, na_o, "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+          "-Wl,-rpath," + os.path.join(rocm, "lib"), "-pthread", "-o", tmp])
+    os.replace(tmp, SAN_EXE)
+    if verbose:
+        print(SAN_EXE)
+    return SAN_EXE
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

@@ -577,37 +577,41 @@ int do_sim(svf_batch* h, int64_t delta) {
         HIPCHK(hipStreamWaitEvent(h->aux, h->fork_ev, 0));
         st_known = h->aux;
     }
+    // launch errors are kept until the second stream has been joined back
+    hipError_t le = hipSuccess;
     if (h->n_stepped > 0) {
         svfk::SimArgs T = S;
         T.list_cap = h->step_cap;
         T.list_resume = 0;
         T.resident = h->res_stepped;
         T.prog = h->d_prog + 1;
-        HIPCHK(svfk::launch_sim(T, G, h->d_lds, true, h->list_stepped,
-                                h->list_stepped ? h->lds_step : h->lds_bytes, st_stepped));
-        if (h->list_stepped && h->step_cap < h->list_stride) {
+        le = svfk::launch_sim(T, G, h->d_lds, true, h->list_stepped,
+                              h->list_stepped ? h->lds_step : h->lds_bytes, st_stepped);
+        if (le == hipSuccess && h->list_stepped && h->step_cap < h->list_stride) {
             // segments whose list outgrew the LDS capacity, up to the same step
             T.list_cap = h->list_stride;
             T.list_resume = 1;
             T.resident = 0;
-            HIPCHK(svfk::launch_sim(T, G, false, true, true, h->lds_step_full, st_stepped));
+            le = svfk::launch_sim(T, G, false, true, true, h->lds_step_full, st_stepped);
         }
     }
-    if (h->n_known > 0) {
-        HIPCHK(svfk::launch_sim(S, G, h->d_lds, false, h->list_known,
-                                h->list_known ? h->lds_list : h->lds_bytes, st_known));
-        if (h->list_known && h->list_cap < h->list_stride) {
+    if (le == hipSuccess && h->n_known > 0) {
+        le = svfk::launch_sim(S, G, h->d_lds, false, h->list_known,
+                              h->list_known ? h->lds_list : h->lds_bytes, st_known);
+        if (le == hipSuccess && h->list_known && h->list_cap < h->list_stride) {
             // segments whose list outgrew the LDS capacity, up to the same step
             S.list_cap = h->list_stride;
             S.list_resume = 1;
             S.resident = 0;
-            HIPCHK(svfk::launch_sim(S, G, false, false, true, h->lds_list_full, st_known));
+            le = svfk::launch_sim(S, G, false, false, true, h->lds_list_full, st_known);
         }
     }
     if (fork) {
         HIPCHK(hipEventRecord(h->join_ev, h->aux));
         HIPCHK(hipStreamWaitEvent(h->stream, h->join_ev, 0));
     }
+    if (le != hipSuccess)
+        return fail(SVF_EHIP, "simulation launch failed: %s", hipGetErrorString(le));
     record_end(h, 1, e0);
     h->sim_launches += 1;
     h->dirty = true;
