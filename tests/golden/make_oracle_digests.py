@@ -1,14 +1,15 @@
 """Write tests/golden/oracle_digests.json: SHA-256 digests of the CPU oracle's
-per-request outputs and its per-instance statistics for sampled instances of
+per-request outputs and its per-instance statistics for every instance of
 the full-size large-queue configuration (64 x 200,000 requests, bursts of
 20,000 every 500 steps, M = 2^21, SVF).
 
 The oracle needs about twenty minutes per instance of that configuration, too
 long to recompute inside a GPU test, so the test compares the GPU's outputs
 for the same instances against these digests.  This script calls only the
-oracle and the workload generator.
+oracle and the workload generator; instances are computed in parallel, one
+thread each, and merged into the file, so it can be run in groups.
 
-    python tests/golden/make_oracle_digests.py [instance ids...]
+    python tests/golden/make_oracle_digests.py [instance ids...]   (default: all 64)
 """
 
 import hashlib
@@ -60,5 +61,5 @@ def main(ids):
 
 
 if __name__ == "__main__":
-    ids = [int(x) for x in sys.argv[1:]] or [0, 1, 2, 3, 21, 42, 63]
+    ids = [int(x) for x in sys.argv[1:]] or list(range(W.CONFIGS[5]["instances"]))
     main(ids)

@@ -6,7 +6,9 @@ statistics.  Small cases run the oracle on every instance; the full-size
 configurations, in the launch configuration the benchmark times, are compared
 on sampled instances (each instance is independent and regenerated from its
 own seed) and checked on all instances through properties that hold at any
-size.
+size; the large-queue configuration is compared on every instance through
+digests of the oracle's outputs (tests/golden/oracle_digests.json), and
+tests/test_gpu_full_parity.py compares every instance of the others.
 """
 
 import hashlib
@@ -669,6 +671,8 @@ def test_full_config5_against_stored_oracle_digests():
     path = os.path.join(GOLDEN, "oracle_digests.json")
     data = json.load(open(path))["cfg5/svf"]
     b = W.config(5)
+    assert sorted(map(int, data["instances"])) == list(range(b.num_instances)), \
+        "the stored digests do not cover every instance"
     say("full config 5: 64 x 200000")
     g = gpu_run(b)["svf"]
     # with known lengths neither run can reach its step budget (the budgets of
