@@ -310,6 +310,53 @@ def max_concurrent(b, res):
     return best
 
 
+def test_ring_in_global_memory():
+    """The ring profile kept in global memory instead of LDS (where the ring
+    and bitmap pass 64 KB and the list does not fit either), forced on both
+    paths; then a long tail without forcing (one request 20,000 steps long per
+    instance: a ring of 32,768 slots, too large for LDS, so the host takes the
+    finish-ordered list)."""
+    env = {"SVFSIM_RING": "global", "SVFSIM_PROFILE": "ring", "SVFSIM_STEP_PROFILE": "ring"}
+    old = {k: os.environ.get(k) for k in env}
+    os.environ.update(env)
+    try:
+        b = W.config(2, instances=12, n=400)
+        say("ring in global memory: config 2 reduced")
+        g = gpu_run(b)
+        for pol in b.policies:
+            compare(b, g[pol], pol, label="gring-cfg2")
+        b3 = W.config(3, instances=8)
+        say("ring in global memory: config 3 reduced (1-bit, evictions)")
+        g3 = gpu_run(b3, chunks=[500, 1, 2000, 10 ** 9])
+        for pol in b3.policies:
+            compare(b3, g3[pol], pol, label="gring-cfg3")
+        assert int(g3["svf1bit"]["stats"]["preemptions"].sum()) > 0
+        r = W.random_small(9, instances=40, n_max=60, s_max=12, o_max=20, M=60, gap_mean=0.3,
+                           plan_noise=True)
+        gr = gpu_run(r)
+        for pol in r.policies:
+            compare(r, gr[pol], pol, label="gring-random")
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    rng = np.random.default_rng(5)
+    parts = []
+    for i in range(6):
+        n = 300
+        a = np.sort(rng.integers(0, 2000, n))
+        o = rng.integers(1, 400, n)
+        o[rng.integers(0, n)] = 20000
+        parts.append({"arrival": a, "prompt": rng.integers(1, 200, n), "output": o})
+    bl = W.assemble("longtail", parts, 40000, ("svf", "sjf", "fcfs"))
+    say("one request 20000 steps long per instance")
+    gl = gpu_run(bl)
+    for pol in bl.policies:
+        compare(bl, gl[pol], pol, label="longtail")
+
+
 @pytest.mark.parametrize("profile", ["ring", "list", "list-lds7", "list-lds64"])
 def test_event_path_both_profiles(profile):
     """The event path keeps the future memory profile either as the ring of
