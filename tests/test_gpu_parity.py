@@ -660,6 +660,32 @@ def test_concurrent_launches_equal_one_stream(monkeypatch):
         compare(b, two[pol], pol, ids=_sample(b.num_instances, 8, 11), label="concurrent")
 
 
+def test_two_handles_on_two_streams_at_once():
+    """Two handles, each on a stream of its own (default priority), launched
+    back to back without synchronising: each owns its buffers, so both give
+    what one handle alone gives (config 3: event-driven and per-step
+    segments, issue priorities on)."""
+    import torch
+    b = W.config(3, instances=48, n=600)
+    alone = gpu_run(b)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    h1 = S.Simulator.from_batch(b, stream=s1.cuda_stream)
+    h2 = S.Simulator.from_batch(b, stream=s2.cuda_stream)
+    try:
+        say("two handles on two streams")
+        h1.run()
+        h2.run()
+        for h in (h1, h2):
+            for slot, pol in enumerate(b.policies):
+                d = h.read(slot)
+                for f in FIELDS:
+                    assert np.array_equal(d[f], alone[pol][f]), (pol, f)
+                assert np.array_equal(h.stats(slot), alone[pol]["stats"]), pol
+    finally:
+        h1.close()
+        h2.close()
+
+
 def test_issue_priorities_do_not_change_results(monkeypatch):
     """More segments than the GPU holds at once (several rounds of resident
     workgroups), on the event and the per-step path: outputs with the waves'
