@@ -660,6 +660,19 @@ def test_concurrent_launches_equal_one_stream(monkeypatch):
         compare(b, two[pol], pol, ids=_sample(b.num_instances, 8, 11), label="concurrent")
 
 
+def test_many_tiny_instances():
+    """100,000 instances of one to eight requests under four policies: 400,000
+    single-wave segments, far more workgroups than wave slots, on both paths
+    (1-bit plans take the per-step one)."""
+    b = W.random_small(21, instances=100000, n_max=8, s_max=6, o_max=10, M=24, gap_mean=0.5,
+                       bits=True)
+    pols = ("svf", "sjf", "fcfs", "svf1bit")
+    say(f"many tiny instances: {b.num_instances} instances, {b.num_requests} requests")
+    g = gpu_run(b, pols)
+    for pol in pols:
+        compare(b, g[pol], pol, label="tiny")
+
+
 def test_two_handles_on_two_streams_at_once():
     """Two handles, each on a stream of its own (default priority), launched
     back to back without synchronising: each owns its buffers, so both give
