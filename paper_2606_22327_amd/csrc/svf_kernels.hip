@@ -1131,7 +1131,6 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
         //    ranked above the blocked head (the lowest waiting rank before
         //    this step; none if nothing was waiting).
         const int old_head = head < 0 ? INT32_MAX : head;
-        const int4 hq0 = hq;
         int new_min = INT32_MAX, n_below = 0;
         int4 nq = make_int4(0, 0, 0, 0);
         for (;;) {
@@ -1180,7 +1179,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                 lds_order();
                 max_fin = max(max_fin, t + q.w);
                 // Once every arrival ranked above the old head is running, the
-                // old head (record known) is next, or nothing is left waiting.
+                // old head is next, or nothing is left waiting.
                 // Before t_f it still does not fit: the profile has only grown
                 // since t_f was computed, which can only delay the release.
                 // (Candidates come in rank order, so the first n_below of them
@@ -1189,10 +1188,7 @@ __device__ void run_known(const SimArgs& P, const Seg& sg, uint64_t* B, uint64_t
                 if (--n_below == 0) {
                     if (old_head == INT32_MAX) { head = -1; break; }
                     if (t < t_f) break;
-                    r = old_head;
-                    q = hq0;
-                    if (cw != (r >> 6)) load_word(r >> 6);
-                    continue;
+                    // the old head is now the lowest waiting rank: found below
                 }
                 if (cbits != 0ull) {
                     r = cw * 64 + __builtin_ctzll(cbits);
