@@ -50,12 +50,16 @@ def kernel_source_digest():
     return hashlib.sha256(data + " ".join(B.GPU_FLAGS).encode()).hexdigest()[:16]
 
 
-def issue_from_profile(workload):
-    """Instructions the simulation kernel issues per launch (rocprofv3 SQ
-    counters SQ_INSTS_SALU and SQ_INSTS_VALU, deterministic for a given kernel
-    and workload), if recorded for this workload and the current kernels; None
-    otherwise (profiles/issue_<workload>.json)."""
-    p = os.path.join(ROOT, "profiles", f"issue_{workload}.json")
+# Knobs that change which kernels run or how: the committed profiles were
+# taken with none of them set, so they do not describe a run that sets one.
+KERNEL_KNOBS = ("SVFSIM_PROFILE", "SVFSIM_STEP_PROFILE", "SVFSIM_RING", "SVFSIM_LIST_LDS_CAP",
+                "SVFSIM_STEP_LDS_CAP", "SVFSIM_ISSUE_PRIO", "SVFSIM_CONCURRENT")
+
+
+def _profile(kind, workload):
+    if any(os.environ.get(k) for k in KERNEL_KNOBS):
+        return None
+    p = os.path.join(ROOT, "profiles", f"{kind}_{workload}.json")
     if not os.path.exists(p):
         return None
     try:
@@ -63,6 +67,17 @@ def issue_from_profile(workload):
     except Exception:
         return None
     if d.get("kernel_source_sha256_16") != kernel_source_digest():
+        return None
+    return d
+
+
+def issue_from_profile(workload):
+    """Instructions the simulation kernel issues per launch (rocprofv3 SQ
+    counters SQ_INSTS_SALU and SQ_INSTS_VALU, deterministic for a given kernel
+    and workload), if recorded for this workload and the current kernels; None
+    otherwise (profiles/issue_<workload>.json)."""
+    d = _profile("issue", workload)
+    if d is None:
         return None
     c = d["counters"]
     return {"salu": float(c["SQ_INSTS_SALU"]), "valu": float(c["SQ_INSTS_VALU"]),
@@ -75,16 +90,8 @@ def traffic_from_profile(workload):
     (FETCH_SIZE and WRITE_SIZE, each scaled by a plain copy kernel's reading),
     if recorded for this workload and for the current kernel source; None
     otherwise (profiles/traffic_<workload>.json)."""
-    p = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
-    if not os.path.exists(p):
-        return None
-    try:
-        d = json.load(open(p))
-    except Exception:
-        return None
-    if d.get("kernel_source_sha256_16") != kernel_source_digest():
-        return None
-    return d.get("bytes_per_launch")
+    d = _profile("traffic", workload)
+    return None if d is None else d.get("bytes_per_launch")
 
 
 def make_batch(cfg, instances, policies, sigma):
