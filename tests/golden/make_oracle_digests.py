@@ -10,6 +10,12 @@ oracle and the workload generator; instances are computed in parallel, one
 thread each, and merged into the file, so it can be run in groups.
 
     python tests/golden/make_oracle_digests.py [instance ids...]   (default: all 64)
+
+With the argument ``pred`` it writes, instead, one digest per block of 1,024
+instances of the heavy-traffic configuration (16,384 x 5,000) planned with
+predicted lengths (sigma 0.5), SVF (about half an hour on 8 threads):
+
+    python tests/golden/make_oracle_digests.py pred [threads]
 """
 
 import hashlib
@@ -60,6 +66,51 @@ def main(ids):
     print(f"wrote {OUT} ({dt:.0f} s)")
 
 
+PRED_KEY = "cfg4-pred0.5/svf"
+PRED_BLOCK = 1024
+STAT_DIGEST_FIELDS = ("makespan", "status", "sum_latency", "request_steps", "peak_mem",
+                      "preemptions", "t_end")
+
+
+def pred_block_digest(start, finish, preempt, admit_seq, stats_cols):
+    """Digest of one block of instances: the four per-request arrays (int32),
+    then the statistics (int64, one column per field of STAT_DIGEST_FIELDS,
+    instance-major)."""
+    h = hashlib.sha256()
+    for a in (start, finish, preempt, admit_seq):
+        h.update(np.ascontiguousarray(a, dtype=np.int32).tobytes())
+    h.update(np.ascontiguousarray(np.stack(stats_cols, axis=1), dtype=np.int64).tobytes())
+    return h.hexdigest()
+
+
+def main_pred(threads):
+    """The heavy-traffic workload (16,384 x 5,000) planned with predicted
+    lengths (sigma 0.5), SVF: one digest per block of PRED_BLOCK instances."""
+    b = W.with_predictor(W.config(4), 0.5)
+    data = json.load(open(OUT)) if os.path.exists(OUT) else {}
+    entry = {"config": W.CONFIG_TITLES[4] + ", predicted lengths (sigma 0.5)",
+             "max_steps": b.max_steps, "block": PRED_BLOCK, "blocks": {}}
+    t0 = time.time()
+    for lo in range(0, b.num_instances, PRED_BLOCK):
+        hi = min(lo + PRED_BLOCK, b.num_instances)
+        sub = b.subset(range(lo, hi))
+        r = oracle.run(sub, "svf", threads=threads)
+        cols = [r["stats"][:, oracle.STAT_FIELDS.index(f)] for f in STAT_DIGEST_FIELDS]
+        entry["blocks"][f"{lo}"] = {
+            "instances": hi - lo,
+            "sha256": pred_block_digest(r["start"], r["finish"], r["preempt"], r["admit_seq"], cols),
+            "preemptions": int(r["preempt"].sum()),
+        }
+        print(f"block {lo}..{hi - 1} done ({time.time() - t0:.0f} s)", flush=True)
+    entry["oracle_seconds"] = round(time.time() - t0, 1)
+    data[PRED_KEY] = entry
+    json.dump(data, open(OUT, "w"), indent=1, sort_keys=True)
+    print(f"wrote {OUT}")
+
+
 if __name__ == "__main__":
-    ids = [int(x) for x in sys.argv[1:]] or list(range(W.CONFIGS[5]["instances"]))
-    main(ids)
+    if sys.argv[1:2] == ["pred"]:
+        main_pred(int(sys.argv[2]) if len(sys.argv) > 2 else (os.cpu_count() or 1))
+    else:
+        ids = [int(x) for x in sys.argv[1:]] or list(range(W.CONFIGS[5]["instances"]))
+        main(ids)

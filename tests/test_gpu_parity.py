@@ -778,8 +778,10 @@ def test_full_config5_against_stored_oracle_digests():
 
 def test_full_config4_predictor_sampled():
     """The full heavy-traffic workload planned with predicted lengths (sigma
-    0.5), in one launch: sampled instances against the oracle, every instance
-    through properties that hold with preemption."""
+    0.5), in one launch: every instance against the oracle through the
+    digests of its outputs stored per block of 1,024 instances
+    (tests/golden/oracle_digests.json), sampled instances directly, and every
+    instance through properties that hold with preemption."""
     b = W.with_predictor(W.config(4), 0.5)
     say(f"full config 4 with predicted lengths: {b.num_instances} instances")
     t0 = time.time()
@@ -793,6 +795,20 @@ def test_full_config4_predictor_sampled():
     assert int(st["preemptions"].sum()) == int(g["svf"]["preempt"].sum()) > 0
     ids = [0, 1, 4095, 8191, 12000, b.num_instances - 1]
     compare(b, g["svf"], "svf", ids=ids, label="pred-full-cfg4")
+    data = json.load(open(os.path.join(GOLDEN, "oracle_digests.json")))["cfg4-pred0.5/svf"]
+    blk = int(data["block"])
+    assert sorted(map(int, data["blocks"])) == list(range(0, b.num_instances, blk)), \
+        "the stored digests do not cover every block"
+    for lo_s, ent in data["blocks"].items():
+        lo = int(lo_s)
+        hi = min(lo + blk, b.num_instances)
+        a0, a1 = int(b.offsets[lo]), int(b.offsets[hi])
+        h = hashlib.sha256()
+        for f in FIELDS:
+            h.update(np.ascontiguousarray(g["svf"][f][a0:a1], dtype=np.int32).tobytes())
+        cols = np.stack([st[f][lo:hi].astype(np.int64) for f in SFIELDS], axis=1)
+        h.update(np.ascontiguousarray(cols, dtype=np.int64).tobytes())
+        assert h.hexdigest() == ent["sha256"], f"instances {lo}..{hi - 1}"
 
 
 def test_poisson_geometric_bounds_and_parity():
