@@ -13,9 +13,11 @@ thread each, and merged into the file, so it can be run in groups.
 
 With the argument ``pred`` it writes, instead, one digest per block of 1,024
 instances of the heavy-traffic configuration (16,384 x 5,000) planned with
-predicted lengths (sigma 0.5), SVF (about half an hour on 8 threads):
+predicted lengths (sigma 0.5), SVF (about half an hour on 8 threads); with
+``cur``, the same configuration under SVF with next-step admission (about
+three hours):
 
-    python tests/golden/make_oracle_digests.py pred [threads]
+    python tests/golden/make_oracle_digests.py pred|cur [threads]
 """
 
 import hashlib
@@ -83,18 +85,32 @@ def pred_block_digest(start, finish, preempt, admit_seq, stats_cols):
     return h.hexdigest()
 
 
-def main_pred(threads):
+# block-digest workloads: name -> (key, policy, description)
+BLOCK_WORKLOADS = {
+    "pred": (PRED_KEY, "svf", ", predicted lengths (sigma 0.5)"),
+    "cur": ("cfg4/svf+cur", "svf+cur", ", next-step admission (SVF_ADMIT_CURRENT)"),
+}
+
+
+def block_batch(mode):
+    if mode == "pred":
+        return W.with_predictor(W.config(4), 0.5)
+    return W.config(4, policies=("svf+cur",))
+
+
+def main_pred(threads, mode="pred"):
     """The heavy-traffic workload (16,384 x 5,000) planned with predicted
-    lengths (sigma 0.5), SVF: one digest per block of PRED_BLOCK instances."""
-    b = W.with_predictor(W.config(4), 0.5)
-    data = json.load(open(OUT)) if os.path.exists(OUT) else {}
-    entry = {"config": W.CONFIG_TITLES[4] + ", predicted lengths (sigma 0.5)",
+    lengths (sigma 0.5) under SVF, or with next-step admission under SVF
+    (mode "cur"): one digest per block of PRED_BLOCK instances."""
+    key, pol, what = BLOCK_WORKLOADS[mode]
+    b = block_batch(mode)
+    entry = {"config": W.CONFIG_TITLES[4] + what,
              "max_steps": b.max_steps, "block": PRED_BLOCK, "blocks": {}}
     t0 = time.time()
     for lo in range(0, b.num_instances, PRED_BLOCK):
         hi = min(lo + PRED_BLOCK, b.num_instances)
         sub = b.subset(range(lo, hi))
-        r = oracle.run(sub, "svf", threads=threads)
+        r = oracle.run(sub, pol, threads=threads)
         cols = [r["stats"][:, oracle.STAT_FIELDS.index(f)] for f in STAT_DIGEST_FIELDS]
         entry["blocks"][f"{lo}"] = {
             "instances": hi - lo,
@@ -103,14 +119,15 @@ def main_pred(threads):
         }
         print(f"block {lo}..{hi - 1} done ({time.time() - t0:.0f} s)", flush=True)
     entry["oracle_seconds"] = round(time.time() - t0, 1)
-    data[PRED_KEY] = entry
+    data = json.load(open(OUT)) if os.path.exists(OUT) else {}
+    data[key] = entry
     json.dump(data, open(OUT, "w"), indent=1, sort_keys=True)
     print(f"wrote {OUT}")
 
 
 if __name__ == "__main__":
-    if sys.argv[1:2] == ["pred"]:
-        main_pred(int(sys.argv[2]) if len(sys.argv) > 2 else (os.cpu_count() or 1))
+    if sys.argv[1:2] in (["pred"], ["cur"]):
+        main_pred(int(sys.argv[2]) if len(sys.argv) > 2 else (os.cpu_count() or 1), sys.argv[1])
     else:
         ids = [int(x) for x in sys.argv[1:]] or list(range(W.CONFIGS[5]["instances"]))
         main(ids)

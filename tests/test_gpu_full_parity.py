@@ -75,3 +75,33 @@ def test_every_instance_equals_the_oracle(cfg, lo):
             ov = r["stats"][:, c].astype(np.int64)
             assert np.array_equal(gv, ov), f"cfg{cfg} {pol} stat {f} in instances {ids[0]}..{ids[-1]}"
         say(f"cfg{cfg} {pol}: instances {ids[0]}..{ids[-1]} equal ({time.time() - t0:.1f}s)")
+
+
+def test_config2_next_step_admission_every_instance():
+    """The current-capacity rule (admission on the next step's memory, with
+    evictions when the running set outgrows M) under SVF, SJF and FCFS on all
+    4,096 instances of config 2, element by element against the oracle."""
+    pols = ("svf+cur", "sjf+cur", "fcfs+cur")
+    b = W.config(2, policies=pols)
+    say(f"config 2 with next-step admission: {b.num_instances} instances x {len(pols)} policies")
+    with S.Simulator.from_batch(b) as sim:
+        sim.run()
+        g = {}
+        for slot, pol in enumerate(pols):
+            d = sim.read(slot)
+            d["stats"] = sim.stats(slot)
+            g[pol] = d
+    for pol in pols:
+        t0 = time.time()
+        r = oracle.run(b, pol, threads=THREADS)
+        for f in FIELDS:
+            if not np.array_equal(g[pol][f], r[f]):
+                k = int(np.nonzero(g[pol][f] != r[f])[0][0])
+                i = int(np.searchsorted(b.offsets, k, side="right") - 1)
+                raise AssertionError(f"{pol} instance {i} field {f}: gpu {int(g[pol][f][k])} "
+                                     f"oracle {int(r[f][k])}")
+        for c, f in enumerate(oracle.STAT_FIELDS):
+            if f in g[pol]["stats"].dtype.names:
+                assert np.array_equal(g[pol]["stats"][f].astype(np.int64), r["stats"][:, c]), (pol, f)
+        assert int(g[pol]["stats"]["preemptions"].sum()) > 0
+        say(f"{pol}: every instance equal ({time.time() - t0:.1f}s)")
