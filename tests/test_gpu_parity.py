@@ -795,20 +795,27 @@ def test_full_config4_predictor_sampled():
     assert int(st["preemptions"].sum()) == int(g["svf"]["preempt"].sum()) > 0
     ids = [0, 1, 4095, 8191, 12000, b.num_instances - 1]
     compare(b, g["svf"], "svf", ids=ids, label="pred-full-cfg4")
-    data = json.load(open(os.path.join(GOLDEN, "oracle_digests.json")))["cfg4-pred0.5/svf"]
+    check_block_digests(b, g["svf"], "cfg4-pred0.5/svf")
+
+
+def check_block_digests(b, res, key):
+    """Every block of instances of ``res`` against the oracle digests stored
+    under ``key`` (tests/golden/make_oracle_digests.py)."""
+    data = json.load(open(os.path.join(GOLDEN, "oracle_digests.json")))[key]
     blk = int(data["block"])
     assert sorted(map(int, data["blocks"])) == list(range(0, b.num_instances, blk)), \
         "the stored digests do not cover every block"
+    st = res["stats"]
     for lo_s, ent in data["blocks"].items():
         lo = int(lo_s)
         hi = min(lo + blk, b.num_instances)
         a0, a1 = int(b.offsets[lo]), int(b.offsets[hi])
         h = hashlib.sha256()
         for f in FIELDS:
-            h.update(np.ascontiguousarray(g["svf"][f][a0:a1], dtype=np.int32).tobytes())
+            h.update(np.ascontiguousarray(res[f][a0:a1], dtype=np.int32).tobytes())
         cols = np.stack([st[f][lo:hi].astype(np.int64) for f in SFIELDS], axis=1)
         h.update(np.ascontiguousarray(cols, dtype=np.int64).tobytes())
-        assert h.hexdigest() == ent["sha256"], f"instances {lo}..{hi - 1}"
+        assert h.hexdigest() == ent["sha256"], f"{key}: instances {lo}..{hi - 1}"
 
 
 def test_poisson_geometric_bounds_and_parity():
