@@ -798,6 +798,24 @@ def test_full_config4_predictor_sampled():
     check_block_digests(b, g["svf"], "cfg4-pred0.5/svf")
 
 
+def test_full_config4_next_step_admission_against_stored_oracle_digests():
+    """The full heavy-traffic workload under SVF with next-step admission (the
+    current-capacity rule: evictions whenever the running set outgrows M), in
+    one launch: every instance against the oracle through the digests stored
+    per block of 1,024 instances, and properties that hold with preemption."""
+    b = W.config(4, policies=("svf+cur",))
+    say(f"full config 4 with next-step admission: {b.num_instances} instances")
+    t0 = time.time()
+    g = gpu_run(b)["svf+cur"]
+    say(f"gpu done in {time.time() - t0:.1f}s")
+    st = g["stats"]
+    assert (st["status"] == 0).all()
+    assert (g["finish"] == g["start"] + b.output).all()
+    assert (st["peak_mem"] <= b.M).all()
+    assert int(st["preemptions"].sum()) == int(g["preempt"].sum()) > 0
+    check_block_digests(b, g, "cfg4/svf+cur")
+
+
 def check_block_digests(b, res, key):
     """Every block of instances of ``res`` against the oracle digests stored
     under ``key`` (tests/golden/make_oracle_digests.py)."""
