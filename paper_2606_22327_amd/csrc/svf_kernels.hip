@@ -1679,9 +1679,14 @@ __device__ void run_stepped(const SimArgs& P, const Seg& sg, uint64_t* B, uint64
                     for (int u = 0; u < 4; ++u) {
                         const int x = base + 64 * u + lane;
                         if (x >= nA) continue;
-                        const long long e = t - kr[u].x;
-                        const long long L = max((long long)qq[u].z, e + 1);
-                        const long long R = (L - e) * qq[u].y + (L * (L + 1) - e * (e + 1)) / 2;
+                        // sum over x = e+1 .. L of (s + x) = (L - e)(2s + L + e + 1) / 2:
+                        // one 32 x 32 -> 64-bit product (L - e < 2^30, and
+                        // 2s + L + e + 1 < 2^32 with s, L, e < 2^30)
+                        const int e = t - kr[u].x;
+                        const int L = max(qq[u].z, e + 1);
+                        const long long R = (long long)(((unsigned long long)(uint32_t)(L - e) *
+                                                         (uint32_t)(2 * (uint32_t)qq[u].y + (uint32_t)L +
+                                                                    (uint32_t)e + 1u)) >> 1);
                         if (R > bestR || (R == bestR && qq[u].x > bestIdx)) {
                             bestR = R;
                             bestIdx = qq[u].x;
